@@ -1,0 +1,154 @@
+/*
+ * hv.h -- C ABI of the device-resident model-integrity path: chunked SHA-256
+ * of weight bytes already in GPU memory, Merkle reduction of the chunk
+ * digests to per-tensor roots and a manifest root, and comparison of a root
+ * with its expected value.  One AMD Instinct MI355X (gfx950), HIP streams.
+ *
+ * The operations follow arXiv 2510.23938:
+ *   - Algorithm 1 ("Streaming Model Verification for Large Models",
+ *     Discussion): a model is cut into ceil(|M| / C) chunks, each chunk is
+ *     hashed on the GPU, the chunk hashes are the leaves of a Merkle tree
+ *     built on the GPU, and the root is compared with the expected value;
+ *   - the Merkle tree is the one of RFC 6962 section 2.1 (cited for the
+ *     paper's Merkle construction, Introduction), the chunk hash is SHA-256
+ *     (FIPS 180-4, the standard hash the paper names);
+ *   - roots are hierarchical (Introduction, "Hierarchical Integrity
+ *     Verification"): per tensor or shard file, then over those roots;
+ *   - the hash runs where the weights live, on the exact device bytes the
+ *     model executes from, so nothing crosses PCIe (Problem Statement,
+ *     TOCTOU discussion);
+ *   - a status plus caller-provided outputs, as the paper's own C ABI does
+ *     (Implementation, the extern "C" verification entry point).
+ *
+ * Conventions for every call:
+ *   - Device pointers are caller-owned (typically torch tensor storage).  The
+ *     library never allocates device memory: scratch comes from a
+ *     caller-provided workspace of the size the *_workspace_bytes call gives.
+ *   - Calls are asynchronous on `stream` unless marked "synchronous".  Input
+ *     bytes must stay valid and unmodified until the stream work completes.
+ *   - All argument checks happen before any work is queued; on a non-OK
+ *     status nothing was launched (except HV_ERR_HIP, which reports a failed
+ *     launch or copy) and hv_last_error() describes the problem.
+ *   - A root mismatch is not an error: hv_verify_root returns HV_OK, *match=0.
+ *   - No global state except a thread-local error string.  Concurrent calls
+ *     on different streams with different workspaces are safe; calls that
+ *     share a workspace must be ordered by the caller.
+ */
+#ifndef HV_H
+#define HV_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HV_OK = 0,
+    HV_ERR_INVALID_ARG = 1, /* bad pointer, size, chunk size or offsets     */
+    HV_ERR_WORKSPACE = 2,   /* workspace NULL or smaller than required       */
+    HV_ERR_HIP = 3          /* a HIP launch or copy failed                   */
+} hv_status;
+
+/* One message: `nbytes` bytes at device address `data` (any alignment).
+ * `data` may be NULL only when nbytes == 0. */
+typedef struct {
+    const void* data;
+    uint64_t nbytes;
+} hv_msg;
+
+enum { HV_DIGEST_BYTES = 32 };
+
+/* Leaf layout (synchronous, host only, touches no device memory).
+ * Chunking (Algorithm 1): a message of L bytes with chunk size C > 0 has
+ * ceil(L / C) leaves (none when L == 0); chunk i covers bytes
+ * [i*C, min((i+1)*C, L)) -- the last chunk is simply shorter.  C == 0 means
+ * one leaf per message, the whole message (also when L == 0).  C must be 0 or
+ * a multiple of 64 (so every chunk but the last is whole SHA-256 blocks).
+ * Leaves are numbered message-major, chunk-ascending.
+ *   seg_offsets: optional (may be NULL), n_msgs + 1 entries: seg_offsets[0] = 0,
+ *                seg_offsets[m+1] - seg_offsets[m] = leaves of message m.
+ *   n_leaves:    required, total leaves.
+ * Errors: HV_ERR_INVALID_ARG for msgs == NULL with n_msgs > 0, a NULL data
+ * pointer with nbytes > 0, a bad C, a NULL n_leaves, or a count overflow. */
+hv_status hv_leaf_layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                         uint64_t* seg_offsets, uint64_t* n_leaves);
+
+/* Workspace bytes hv_hash_chunks needs for n_msgs messages with n_leaves
+ * leaves in total (from hv_leaf_layout). */
+size_t hv_hash_workspace_bytes(uint32_t n_msgs, uint64_t n_leaves);
+
+/* Chunk digests (Algorithm 1's per-chunk GPU hash): leaf_digests[j] =
+ * SHA-256(chunk j) per FIPS 180-4, 32 bytes each in the standard big-endian
+ * byte order, leaves numbered as in hv_leaf_layout.
+ *   msgs:         host array of n_msgs device messages (read during the call;
+ *                 the descriptors are copied to the workspace).
+ *   chunk_bytes:  0 or a multiple of 64.
+ *   leaf_digests: device, n_leaves * 32 bytes, caller-owned, written.
+ *   workspace:    device, >= hv_hash_workspace_bytes(n_msgs, n_leaves) bytes,
+ *                 256-byte aligned; contents are scratch.
+ * Errors: as hv_leaf_layout, plus leaf_digests == NULL with n_leaves > 0,
+ * HV_ERR_WORKSPACE, HV_ERR_HIP. */
+hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                         uint8_t* leaf_digests, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
+/* Workspace bytes hv_merkle_reduce needs for n_nodes entries in n_seg
+ * segments. */
+size_t hv_merkle_workspace_bytes(uint64_t n_nodes, uint32_t n_seg);
+
+/* Segmented Merkle Tree Hash (RFC 6962 section 2.1; Algorithm 1's "construct
+ * Merkle tree from leaf_hashes"): for every segment s,
+ *   roots[s] = MTH(nodes[seg_offsets[s] .. seg_offsets[s+1]))
+ * with MTH({}) = SHA-256(""), MTH({d}) = SHA-256(0x00 || d) and
+ * MTH(D[0:n]) = SHA-256(0x01 || MTH(D[0:k]) || MTH(D[k:n])), k the largest
+ * power of two below n.  Entries are 32-byte values (chunk digests, or
+ * segment roots for a manifest over tensors -- the hierarchical roots).
+ *   nodes:       device, seg_offsets[n_seg] * 32 bytes, read only.
+ *   seg_offsets: host, n_seg + 1 entries, seg_offsets[0] == 0, non-decreasing.
+ *   roots:       device, n_seg * 32 bytes, written.
+ *   workspace:   device, >= hv_merkle_workspace_bytes(seg_offsets[n_seg], n_seg).
+ * Errors: HV_ERR_INVALID_ARG for n_seg == 0, NULL pointers, offsets that do
+ * not start at 0 or decrease; HV_ERR_WORKSPACE; HV_ERR_HIP. */
+hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg,
+                           uint8_t* roots, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream);
+
+/* Workspace bytes hv_verify_root needs (a few bytes for the device flag). */
+size_t hv_verify_workspace_bytes(void);
+
+/* Root comparison (Algorithm 1's last step), synchronous on `stream`:
+ * *match = 1 when the 32 device bytes at `root` equal `expected`, else 0.
+ * The comparison runs on the GPU over all 32 bytes without an early exit;
+ * only the 4-byte flag crosses to the host.
+ *   root:     device, 32 bytes.   expected: host, 32 bytes.   match: host.
+ *   workspace: device, >= hv_verify_workspace_bytes() bytes.
+ * Errors: HV_ERR_INVALID_ARG for NULL pointers; HV_ERR_WORKSPACE; HV_ERR_HIP. */
+hv_status hv_verify_root(const uint8_t* root, const uint8_t expected[32], int* match,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Per-entry comparison for localising a mismatch (asynchronous):
+ * mismatch[i] = 1 when roots[i] (32 bytes) differs from expected[i], else 0.
+ *   roots, expected: device, n * 32 bytes.   mismatch: device, n uint32.
+ * Errors: HV_ERR_INVALID_ARG for NULL pointers with n > 0; HV_ERR_HIP. */
+hv_status hv_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32_t n,
+                           uint32_t* mismatch, hipStream_t stream);
+
+/* Detail string for the last non-OK status returned on this thread. */
+const char* hv_last_error(void);
+
+/* Kernel timing for measurement.  When enabled (per thread), hv_hash_chunks
+ * records HIP events on `stream` around its SHA-256 leaf kernel, and
+ * hv_leaf_kernel_ms() waits for the last such pair and returns the elapsed
+ * milliseconds.  Off by default; costs two event records per call when on.
+ * Errors: HV_ERR_INVALID_ARG if no timed call was made on this thread. */
+hv_status hv_set_kernel_timing(int enable);
+hv_status hv_leaf_kernel_ms(float* ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HV_H */

@@ -1,0 +1,33 @@
+/*
+ * hv_inspect.h -- inspection entry point for tests of the chunk scheduler.
+ *
+ * hv_leaf_schedule runs the same device-side scheduling hv_hash_chunks runs
+ * (Algorithm 1's chunking: ceil(|M| / C) chunks per message, the last one
+ * shorter) and copies the resulting leaf table to the host, so a test can
+ * check that every chunk appears exactly once, with the right source range
+ * and output slot, in non-increasing order of SHA-256 block count.  It does
+ * not hash.  Synchronous on `stream`.
+ *
+ *   msgs, n_msgs, chunk_bytes, workspace, workspace_bytes: as hv_hash_chunks.
+ *   table: host, n_leaves * 3 uint64 values, written in schedule order as
+ *          {source device address, byte length, leaf index} per leaf.
+ * Errors: as hv_hash_chunks (HV_ERR_INVALID_ARG for a NULL table with
+ * n_leaves > 0).
+ */
+#ifndef HV_INSPECT_H
+#define HV_INSPECT_H
+
+#include "hv.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t* table,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HV_INSPECT_H */

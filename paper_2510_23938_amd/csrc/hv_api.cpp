@@ -1,0 +1,341 @@
+// hv_api.cpp -- the C ABI declared in include/hv.h: argument validation,
+// workspace carving and the launch sequence on the caller's stream.  All
+// arithmetic on message bytes and digests runs in the kernels; the host only
+// plans (offsets and counts from the descriptor array) and launches.
+#include "hv.h"
+#include "hv_inspect.h"
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+#include "hv_kernels.h"
+
+namespace {
+
+thread_local char g_error[512] = "";
+
+hv_status fail(hv_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_error, sizeof g_error, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+hv_status hip_fail(hipError_t e, const char* what) {
+    return fail(HV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Largest leaf count one call accepts: the hash grid is 256 lanes per block
+// in a 32-bit block index.
+constexpr uint64_t kMaxLeaves = (uint64_t)1 << 38;
+
+// Carves consecutive 256-byte-aligned regions out of a workspace.
+struct Carver {
+    uint8_t* base;
+    size_t used = 0;
+    explicit Carver(void* b) : base(static_cast<uint8_t*>(b)) {}
+    template <typename T>
+    T* take(size_t count) {
+        T* p = reinterpret_cast<T*>(base ? base + used : nullptr);
+        used += round_up(count * sizeof(T));
+        return p;
+    }
+};
+
+struct HashLayout {
+    hv::MsgDesc* msgs;
+    hv::Pair* cnt;
+    hv::Pair* off;
+    hv::Pair* partials;
+    uint64_t* hist;
+    hv::LeafDesc* desc;
+    size_t bytes;
+};
+
+HashLayout hash_layout(void* ws, uint32_t n_msgs, uint64_t n_leaves) {
+    Carver c(ws);
+    HashLayout L;
+    L.msgs = c.take<hv::MsgDesc>(n_msgs);
+    L.cnt = c.take<hv::Pair>(n_msgs);
+    L.off = c.take<hv::Pair>((size_t)n_msgs + 1);
+    L.partials = c.take<hv::Pair>(hv::scan_partials_count(n_msgs));
+    L.hist = c.take<uint64_t>(hv::kSortBuckets);
+    L.desc = c.take<hv::LeafDesc>(n_leaves);
+    L.bytes = c.used;
+    return L;
+}
+
+// Leaf counts of a message list; fills seg_offsets when given.
+hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_offsets, uint64_t* n_leaves,
+                 uint64_t* n_full) {
+    if (n_msgs > 0 && msgs == nullptr) return fail(HV_ERR_INVALID_ARG, "msgs is NULL with n_msgs = %u", n_msgs);
+    if (C % 64 != 0) return fail(HV_ERR_INVALID_ARG, "chunk_bytes = %llu is not 0 or a multiple of 64",
+                                 (unsigned long long)C);
+    uint64_t total = 0, full = 0;
+    if (seg_offsets) seg_offsets[0] = 0;
+    for (uint32_t m = 0; m < n_msgs; ++m) {
+        const uint64_t len = msgs[m].nbytes;
+        if (len > 0 && msgs[m].data == nullptr)
+            return fail(HV_ERR_INVALID_ARG, "message %u has NULL data and %llu bytes", m, (unsigned long long)len);
+        if ((uintptr_t)msgs[m].data + len < (uintptr_t)msgs[m].data)
+            return fail(HV_ERR_INVALID_ARG, "message %u wraps the address space", m);
+        uint64_t leaves;
+        if (C == 0) {
+            leaves = 1;
+        } else {
+            leaves = len / C + (len % C != 0);
+            full += len / C;
+        }
+        if (total + leaves < total) return fail(HV_ERR_INVALID_ARG, "leaf count overflows");
+        total += leaves;
+        if (seg_offsets) seg_offsets[m + 1] = total;
+    }
+    *n_leaves = total;
+    if (n_full) *n_full = full;
+    return HV_OK;
+}
+
+struct Timing {
+    bool enabled = false;
+    bool have = false;
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+thread_local Timing g_timing;
+
+// Merkle plan: O[0] = segment offsets, O[k][s] = first output node of segment
+// s after launch k (each segment gets max(1, ceil(count / 512)) tiles).  The
+// last row is 0, 1, ..., n_seg: one node (the root) per segment.
+constexpr int kMaxLaunches = 8;  // ceil(64 / 9): a 64-bit leaf count needs at most 8
+
+struct MerkleLayout {
+    uint64_t* table;
+    uint8_t* ping;
+    uint8_t* pong;
+    size_t bytes;
+};
+
+uint64_t tiles_bound(uint64_t n_nodes, uint32_t n_seg) {
+    return n_nodes / hv::kTileNodes + (uint64_t)n_seg + 1;
+}
+
+MerkleLayout merkle_layout(void* ws, uint64_t n_nodes, uint32_t n_seg) {
+    Carver c(ws);
+    MerkleLayout L;
+    L.table = c.take<uint64_t>((size_t)(kMaxLaunches + 1) * ((size_t)n_seg + 1));
+    const uint64_t nb = tiles_bound(n_nodes, n_seg);
+    L.ping = c.take<uint8_t>(nb * 32);
+    L.pong = c.take<uint8_t>(nb * 32);
+    L.bytes = c.used;
+    return L;
+}
+
+// Validation plus the scheduling kernels shared by hv_hash_chunks and
+// hv_leaf_schedule.  On HV_OK the leaf table is queued into L.desc.
+hv_status schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, bool need_out, const void* out,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream, HashLayout* L_out,
+                   uint64_t* n_leaves_out) {
+    uint64_t n_leaves = 0, n_full = 0;
+    hv_status st = layout(msgs, n_msgs, chunk_bytes, nullptr, &n_leaves, &n_full);
+    if (st != HV_OK) return st;
+    if (n_leaves > kMaxLeaves) return fail(HV_ERR_INVALID_ARG, "%llu leaves exceed the per-call limit",
+                                           (unsigned long long)n_leaves);
+    if (need_out && n_leaves > 0 && out == nullptr) return fail(HV_ERR_INVALID_ARG, "leaf_digests is NULL");
+    if (need_out && (uintptr_t)out % 16 != 0) return fail(HV_ERR_INVALID_ARG, "leaf_digests is not 16-byte aligned");
+    if (!need_out && n_leaves > 0 && out == nullptr) return fail(HV_ERR_INVALID_ARG, "table is NULL");
+    const HashLayout need = hash_layout(nullptr, n_msgs, n_leaves);
+    if (workspace == nullptr || workspace_bytes < need.bytes)
+        return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu%s", need.bytes, workspace_bytes,
+                    workspace ? "" : " (NULL)");
+    if ((uintptr_t)workspace % kAlign != 0) return fail(HV_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    *n_leaves_out = n_leaves;
+    *L_out = hash_layout(workspace, n_msgs, n_leaves);
+    if (n_msgs == 0) return HV_OK;
+
+    const HashLayout& L = *L_out;
+    static_assert(sizeof(hv_msg) == sizeof(hv::MsgDesc), "hv_msg layout");
+    hipError_t e = hipMemcpyAsync(L.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail(e, "descriptor upload");
+    if ((e = hv::launch_sched_count(L.msgs, n_msgs, chunk_bytes, L.cnt, stream)) != hipSuccess)
+        return hip_fail(e, "count kernel");
+    if ((e = hv::launch_scan_pairs(L.cnt, L.off, n_msgs, L.partials, stream)) != hipSuccess)
+        return hip_fail(e, "scan kernels");
+    if (n_full > 0 &&
+        (e = hv::launch_sched_full(L.msgs, L.off, n_msgs, chunk_bytes, n_full, L.desc, stream)) != hipSuccess)
+        return hip_fail(e, "full-chunk kernel");
+    if (n_leaves > n_full &&
+        (e = hv::launch_sched_tails(L.msgs, L.off, n_msgs, chunk_bytes, n_full, L.hist, L.desc, stream)) !=
+            hipSuccess)
+        return hip_fail(e, "tail sort kernels");
+    return HV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hv_last_error(void) { return g_error; }
+
+hv_status hv_leaf_layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t* seg_offsets,
+                         uint64_t* n_leaves) {
+    if (n_leaves == nullptr) return fail(HV_ERR_INVALID_ARG, "n_leaves is NULL");
+    return layout(msgs, n_msgs, chunk_bytes, seg_offsets, n_leaves, nullptr);
+}
+
+size_t hv_hash_workspace_bytes(uint32_t n_msgs, uint64_t n_leaves) {
+    return hash_layout(nullptr, n_msgs, n_leaves).bytes;
+}
+
+hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint8_t* leaf_digests,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    HashLayout L;
+    uint64_t n_leaves = 0;
+    hv_status st = schedule(msgs, n_msgs, chunk_bytes, true, leaf_digests, workspace, workspace_bytes, stream, &L,
+                            &n_leaves);
+    if (st != HV_OK || n_leaves == 0) return st;
+
+    hipError_t e;
+    Timing& T = g_timing;
+    if (T.enabled) {
+        if (!T.start && (e = hipEventCreate(&T.start)) != hipSuccess) return hip_fail(e, "event create");
+        if (!T.stop && (e = hipEventCreate(&T.stop)) != hipSuccess) return hip_fail(e, "event create");
+        if ((e = hipEventRecord(T.start, stream)) != hipSuccess) return hip_fail(e, "event record");
+    }
+    if ((e = hv::launch_sha256_leaves(L.desc, n_leaves, leaf_digests, stream)) != hipSuccess)
+        return hip_fail(e, "sha256 leaf kernel");
+    if (T.enabled) {
+        if ((e = hipEventRecord(T.stop, stream)) != hipSuccess) return hip_fail(e, "event record");
+        T.have = true;
+    }
+    return HV_OK;
+}
+
+hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t* table,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    HashLayout L;
+    uint64_t n_leaves = 0;
+    hv_status st = schedule(msgs, n_msgs, chunk_bytes, false, table, workspace, workspace_bytes, stream, &L,
+                            &n_leaves);
+    if (st != HV_OK || n_leaves == 0) return st;
+    static_assert(sizeof(hv::LeafDesc) == 3 * sizeof(uint64_t), "leaf table layout");
+    hipError_t e = hipMemcpyAsync(table, L.desc, n_leaves * sizeof(hv::LeafDesc), hipMemcpyDeviceToHost, stream);
+    if (e != hipSuccess) return hip_fail(e, "table copy");
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "stream synchronize");
+    return HV_OK;
+}
+
+size_t hv_merkle_workspace_bytes(uint64_t n_nodes, uint32_t n_seg) {
+    return merkle_layout(nullptr, n_nodes, n_seg).bytes;
+}
+
+hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg, uint8_t* roots,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (n_seg == 0) return fail(HV_ERR_INVALID_ARG, "n_seg is 0");
+    if (seg_offsets == nullptr) return fail(HV_ERR_INVALID_ARG, "seg_offsets is NULL");
+    if (roots == nullptr) return fail(HV_ERR_INVALID_ARG, "roots is NULL");
+    if (seg_offsets[0] != 0) return fail(HV_ERR_INVALID_ARG, "seg_offsets[0] = %llu, not 0",
+                                         (unsigned long long)seg_offsets[0]);
+    for (uint32_t s = 0; s < n_seg; ++s)
+        if (seg_offsets[s + 1] < seg_offsets[s])
+            return fail(HV_ERR_INVALID_ARG, "seg_offsets decreases at segment %u", s);
+    const uint64_t n_nodes = seg_offsets[n_seg];
+    if (n_nodes > kMaxLeaves) return fail(HV_ERR_INVALID_ARG, "%llu entries exceed the per-call limit",
+                                          (unsigned long long)n_nodes);
+    if (n_nodes > 0 && nodes == nullptr) return fail(HV_ERR_INVALID_ARG, "nodes is NULL");
+    if ((uintptr_t)nodes % 16 != 0 || (uintptr_t)roots % 16 != 0)
+        return fail(HV_ERR_INVALID_ARG, "nodes and roots must be 16-byte aligned");
+    const MerkleLayout need = merkle_layout(nullptr, n_nodes, n_seg);
+    if (workspace == nullptr || workspace_bytes < need.bytes)
+        return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu%s", need.bytes, workspace_bytes,
+                    workspace ? "" : " (NULL)");
+    if ((uintptr_t)workspace % kAlign != 0) return fail(HV_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+
+    // Plan on the host: rows of n_seg + 1 offsets, one per launch level.
+    const size_t row = (size_t)n_seg + 1;
+    std::vector<uint64_t> table(seg_offsets, seg_offsets + row);
+    int launches = 0;
+    for (;;) {
+        const uint64_t* prev = &table[(size_t)launches * row];
+        std::vector<uint64_t> next(row);
+        next[0] = 0;
+        bool more = false;
+        for (uint32_t s = 0; s < n_seg; ++s) {
+            const uint64_t c = prev[s + 1] - prev[s];
+            const uint64_t tiles = c <= (uint64_t)hv::kTileNodes ? 1 : (c + hv::kTileNodes - 1) / hv::kTileNodes;
+            if (tiles > 1) more = true;
+            next[s + 1] = next[s] + tiles;
+        }
+        table.insert(table.end(), next.begin(), next.end());
+        ++launches;
+        if (!more) break;
+        if (launches == kMaxLaunches) return fail(HV_ERR_INVALID_ARG, "tree too deep");
+    }
+
+    const MerkleLayout L = merkle_layout(workspace, n_nodes, n_seg);
+    hipError_t e = hipMemcpyAsync(L.table, table.data(), table.size() * sizeof(uint64_t), hipMemcpyHostToDevice,
+                                  stream);
+    if (e != hipSuccess) return hip_fail(e, "plan upload");
+    const uint8_t* in = nodes;
+    for (int k = 1; k <= launches; ++k) {
+        uint8_t* out = k == launches ? roots : (k % 2 ? L.ping : L.pong);
+        const uint64_t* in_off = L.table + (size_t)(k - 1) * row;
+        const uint64_t* tile_off = L.table + (size_t)k * row;
+        const uint64_t n_tiles = table[(size_t)k * row + n_seg];
+        if ((e = hv::launch_merkle_tiles(in, out, in_off, tile_off, n_seg, n_tiles, k == 1, stream)) != hipSuccess)
+            return hip_fail(e, "merkle kernel");
+        in = out;
+    }
+    return HV_OK;
+}
+
+size_t hv_verify_workspace_bytes(void) { return kAlign; }
+
+hv_status hv_verify_root(const uint8_t* root, const uint8_t expected[32], int* match, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+    if (root == nullptr || expected == nullptr || match == nullptr)
+        return fail(HV_ERR_INVALID_ARG, "root, expected and match must be non-NULL");
+    if (workspace == nullptr || workspace_bytes < hv_verify_workspace_bytes())
+        return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes", hv_verify_workspace_bytes());
+    uint32_t exp_le[8];
+    memcpy(exp_le, expected, 32);
+    uint32_t* flag = static_cast<uint32_t*>(workspace);
+    hipError_t e = hv::launch_verify_root(root, exp_le, flag, stream);
+    if (e != hipSuccess) return hip_fail(e, "verify kernel");
+    uint32_t host_flag = 0;
+    if ((e = hipMemcpyAsync(&host_flag, flag, sizeof host_flag, hipMemcpyDeviceToHost, stream)) != hipSuccess)
+        return hip_fail(e, "flag copy");
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "stream synchronize");
+    *match = host_flag == 1 ? 1 : 0;
+    return HV_OK;
+}
+
+hv_status hv_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32_t n, uint32_t* mismatch,
+                           hipStream_t stream) {
+    if (n > 0 && (roots == nullptr || expected == nullptr || mismatch == nullptr))
+        return fail(HV_ERR_INVALID_ARG, "roots, expected and mismatch must be non-NULL");
+    hipError_t e = hv::launch_compare_roots(roots, expected, n, mismatch, stream);
+    if (e != hipSuccess) return hip_fail(e, "compare kernel");
+    return HV_OK;
+}
+
+hv_status hv_set_kernel_timing(int enable) {
+    g_timing.enabled = enable != 0;
+    return HV_OK;
+}
+
+hv_status hv_leaf_kernel_ms(float* ms) {
+    if (ms == nullptr) return fail(HV_ERR_INVALID_ARG, "ms is NULL");
+    if (!g_timing.have) return fail(HV_ERR_INVALID_ARG, "no timed hv_hash_chunks call on this thread");
+    hipError_t e = hipEventSynchronize(g_timing.stop);
+    if (e != hipSuccess) return hip_fail(e, "event synchronize");
+    if ((e = hipEventElapsedTime(ms, g_timing.start, g_timing.stop)) != hipSuccess) return hip_fail(e, "elapsed");
+    return HV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,270 @@
+"""Python binding of ``include/hv.h``: argument marshalling only.
+
+Every step of the path (chunk scheduling, SHA-256, Merkle levels, root
+comparison) runs in the HIP kernels of ``libhv.so``; this module turns torch
+device tensors into (pointer, length) descriptors, allocates caller-owned
+outputs and workspaces with torch, passes torch's current HIP stream, and
+turns error statuses into exceptions.  There is no CPU fallback: if the
+library is missing, importing this module fails.
+
+Names follow the C ABI:
+
+* ``hv_leaf_layout(ptrs, lens, C)``        -> (seg_offsets, n_leaves)
+* ``hv_hash_chunks(msgs, C)``              -> (leaf digests [n, 32] uint8, seg_offsets)
+* ``hv_merkle_reduce(nodes, seg_offsets)`` -> roots [n_seg, 32] uint8
+* ``hv_verify_root(root, expected)``       -> bool
+* ``hv_compare_roots(roots, expected)``    -> mismatch flags [n] (int32)
+
+plus compositions used by callers: ``manifest_root`` (per-tensor roots, then
+one root over them in the given order -- the paper's hierarchical roots) and
+``verify`` (raises ``VerificationError`` on a mismatch, as the paper's
+loader does when a model fails its check).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # loads the HIP runtime libhv.so binds to
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhv.so")
+
+HV_OK, HV_ERR_INVALID_ARG, HV_ERR_WORKSPACE, HV_ERR_HIP = 0, 1, 2, 3
+_STATUS = {1: "HV_ERR_INVALID_ARG", 2: "HV_ERR_WORKSPACE", 3: "HV_ERR_HIP"}
+
+# exported symbols, in the order include/hv.h declares them
+EXPORTS = (
+    "hv_leaf_layout", "hv_hash_workspace_bytes", "hv_hash_chunks", "hv_merkle_workspace_bytes",
+    "hv_merkle_reduce", "hv_verify_workspace_bytes", "hv_verify_root", "hv_compare_roots",
+    "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
+    "hv_leaf_schedule",  # include/hv_inspect.h
+)
+
+
+class HVError(RuntimeError):
+    """A non-OK status from libhv; ``status`` holds the code."""
+
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+class VerificationError(Exception):
+    """The computed root differs from the expected root."""
+
+
+class hv_msg(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("nbytes", ctypes.c_uint64)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() (no CPU fallback exists)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, u32, u64, sz = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_size_t
+    sig = {
+        "hv_leaf_layout": ([vp, u32, u64, vp, vp], ctypes.c_int),
+        "hv_hash_workspace_bytes": ([u32, u64], sz),
+        "hv_hash_chunks": ([vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
+        "hv_merkle_workspace_bytes": ([u64, u32], sz),
+        "hv_merkle_reduce": ([vp, vp, u32, vp, vp, sz, vp], ctypes.c_int),
+        "hv_verify_workspace_bytes": ([], sz),
+        "hv_verify_root": ([vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "hv_compare_roots": ([vp, vp, u32, vp, vp], ctypes.c_int),
+        "hv_last_error": ([], ctypes.c_char_p),
+        "hv_set_kernel_timing": ([ctypes.c_int], ctypes.c_int),
+        "hv_leaf_kernel_ms": ([vp], ctypes.c_int),
+        "hv_leaf_schedule": ([vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes, f.restype = args, res
+    return lib
+
+
+lib = _load()
+
+
+def _check(status: int):
+    if status != HV_OK:
+        raise HVError(status, lib.hv_last_error().decode("utf-8", "replace"))
+
+
+def _stream(device=None) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+class Workspace:
+    """A growable device byte buffer handed to the library as scratch."""
+
+    def __init__(self, device="cuda"):
+        self.device = torch.device(device)
+        self.buf = None
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        nbytes = max(int(nbytes), 256)
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return self.buf
+
+
+def _msg_array(ptrs: np.ndarray, lens: np.ndarray) -> np.ndarray:
+    """hv_msg[n] as a (n, 2) uint64 array (data, nbytes)."""
+    arr = np.empty((len(lens), 2), dtype=np.uint64)
+    arr[:, 0] = np.asarray(ptrs, dtype=np.uint64)
+    arr[:, 1] = np.asarray(lens, dtype=np.uint64)
+    return arr
+
+
+def messages_of(tensors) -> tuple:
+    """(ptrs, lens) of contiguous device tensors' bytes, in the given order."""
+    ptrs, lens = [], []
+    for t in tensors:
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous: the bytes hashed are the bytes stored")
+        ptrs.append(t.data_ptr())
+        lens.append(t.numel() * t.element_size())
+    return np.array(ptrs, dtype=np.uint64), np.array(lens, dtype=np.uint64)
+
+
+def _ptr_len(msgs):
+    if hasattr(msgs, "ptrs") and hasattr(msgs, "lens"):
+        return np.asarray(msgs.ptrs, dtype=np.uint64), np.asarray(msgs.lens, dtype=np.uint64)
+    if isinstance(msgs, tuple) and len(msgs) == 2 and isinstance(msgs[0], np.ndarray):
+        return msgs
+    return messages_of(msgs)
+
+
+def hv_leaf_layout(ptrs, lens, chunk_bytes: int):
+    arr = _msg_array(ptrs, lens)
+    n = len(arr)
+    seg = np.zeros(n + 1, dtype=np.uint64)
+    n_leaves = ctypes.c_uint64(0)
+    _check(lib.hv_leaf_layout(arr.ctypes.data if n else None, n, chunk_bytes, seg.ctypes.data,
+                              ctypes.byref(n_leaves)))
+    return seg, int(n_leaves.value)
+
+
+def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace | None = None, out=None):
+    """Leaf digests of ``msgs`` (tensors, a (ptrs, lens) pair, or an object with
+    ``ptrs``/``lens``): ([n_leaves, 32] uint8 device tensor, seg_offsets)."""
+    ptrs, lens = _ptr_len(msgs)
+    seg, n_leaves = hv_leaf_layout(ptrs, lens, chunk_bytes)
+    arr = _msg_array(ptrs, lens)
+    n = len(arr)
+    dev = torch.device(device)
+    if out is None:
+        out = torch.empty((n_leaves, 32), dtype=torch.uint8, device=dev)
+    ws = (workspace or Workspace(dev)).get(lib.hv_hash_workspace_bytes(n, n_leaves))
+    _check(lib.hv_hash_chunks(arr.ctypes.data if n else None, n, chunk_bytes, out.data_ptr() if n_leaves else None,
+                              ws.data_ptr(), ws.numel(), _stream(dev)))
+    return out, seg
+
+
+def hv_merkle_reduce(nodes: torch.Tensor, seg_offsets, workspace: Workspace | None = None, out=None):
+    """Per-segment RFC 6962 roots of ``nodes`` ([n, 32] uint8 device tensor)."""
+    seg = np.ascontiguousarray(seg_offsets, dtype=np.uint64)
+    n_seg = len(seg) - 1
+    if out is None:
+        out = torch.empty((max(n_seg, 0), 32), dtype=torch.uint8, device=nodes.device)
+    ws = (workspace or Workspace(nodes.device)).get(lib.hv_merkle_workspace_bytes(int(seg[-1]), n_seg))
+    _check(lib.hv_merkle_reduce(nodes.data_ptr() if nodes.numel() else None, seg.ctypes.data, n_seg,
+                                out.data_ptr() if n_seg else None, ws.data_ptr(), ws.numel(),
+                                _stream(nodes.device)))
+    return out
+
+
+def hv_verify_root(root: torch.Tensor, expected: bytes, workspace: Workspace | None = None) -> bool:
+    """The 32 device bytes of ``root`` equal ``expected`` (compared on the GPU)."""
+    exp = (ctypes.c_uint8 * 32).from_buffer_copy(bytes(expected))
+    match = ctypes.c_int(-1)
+    ws = (workspace or Workspace(root.device)).get(lib.hv_verify_workspace_bytes())
+    _check(lib.hv_verify_root(root.data_ptr(), exp, ctypes.byref(match), ws.data_ptr(), ws.numel(),
+                              _stream(root.device)))
+    return match.value == 1
+
+
+def hv_compare_roots(roots: torch.Tensor, expected: torch.Tensor) -> torch.Tensor:
+    """int32 [n]: 1 where roots[i] differs from expected[i] (both [n, 32] device)."""
+    n = roots.shape[0]
+    mism = torch.empty(n, dtype=torch.int32, device=roots.device)
+    _check(lib.hv_compare_roots(roots.data_ptr(), expected.data_ptr(), n, mism.data_ptr(), _stream(roots.device)))
+    return mism
+
+
+def hv_leaf_schedule(msgs, chunk_bytes: int, device="cuda") -> np.ndarray:
+    """The scheduler's leaf table, in schedule order: uint64 [n_leaves, 3] of
+    (source address, byte length, leaf index).  For tests of the scheduler."""
+    ptrs, lens = _ptr_len(msgs)
+    _, n_leaves = hv_leaf_layout(ptrs, lens, chunk_bytes)
+    arr = _msg_array(ptrs, lens)
+    n = len(arr)
+    table = np.zeros((n_leaves, 3), dtype=np.uint64)
+    dev = torch.device(device)
+    ws = Workspace(dev).get(lib.hv_hash_workspace_bytes(n, n_leaves))
+    _check(lib.hv_leaf_schedule(arr.ctypes.data if n else None, n, chunk_bytes,
+                                table.ctypes.data if n_leaves else None, ws.data_ptr(), ws.numel(), _stream(dev)))
+    return table
+
+
+def set_kernel_timing(enable: bool):
+    _check(lib.hv_set_kernel_timing(1 if enable else 0))
+
+
+def leaf_kernel_ms() -> float:
+    ms = ctypes.c_float(0.0)
+    _check(lib.hv_leaf_kernel_ms(ctypes.byref(ms)))
+    return float(ms.value)
+
+
+class Verifier:
+    """Reusable workspaces for repeated hash -> per-message roots -> manifest -> verify."""
+
+    def __init__(self, device="cuda"):
+        self.device = torch.device(device)
+        self.ws_hash = Workspace(self.device)
+        self.ws_tree = Workspace(self.device)
+        self.ws_manifest = Workspace(self.device)
+        self.ws_verify = Workspace(self.device)
+
+    def leaf_digests(self, msgs, chunk_bytes: int):
+        return hv_hash_chunks(msgs, chunk_bytes, self.device, self.ws_hash)
+
+    def roots(self, msgs, chunk_bytes: int):
+        """(per-message roots [n, 32], leaf digests, seg_offsets)."""
+        leaves, seg = self.leaf_digests(msgs, chunk_bytes)
+        return hv_merkle_reduce(leaves, seg, self.ws_tree), leaves, seg
+
+    def manifest_root(self, msgs, chunk_bytes: int) -> torch.Tensor:
+        """One root over the per-message roots, in message order ([1, 32] device)."""
+        roots, _, _ = self.roots(msgs, chunk_bytes)
+        return hv_merkle_reduce(roots, np.array([0, roots.shape[0]], dtype=np.uint64), self.ws_manifest)
+
+    def single_tree_root(self, msgs, chunk_bytes: int) -> torch.Tensor:
+        """One root over all leaf digests of all messages ([1, 32] device)."""
+        leaves, _ = self.leaf_digests(msgs, chunk_bytes)
+        return hv_merkle_reduce(leaves, np.array([0, leaves.shape[0]], dtype=np.uint64), self.ws_tree)
+
+    def verify_root(self, root: torch.Tensor, expected: bytes) -> bool:
+        return hv_verify_root(root.reshape(-1)[:32], expected, self.ws_verify)
+
+
+def manifest_root(named_tensors, chunk_bytes: int) -> bytes:
+    """Manifest root of {name: tensor} (byte-wise name order) or [(name, tensor)] (given order)."""
+    items = sorted(named_tensors.items(), key=lambda kv: kv[0].encode("utf-8")) \
+        if isinstance(named_tensors, dict) else list(named_tensors)
+    dev = items[0][1].device if items else torch.device("cuda")
+    root = Verifier(dev).manifest_root([t for _, t in items], chunk_bytes)
+    return bytes(root.cpu().numpy().reshape(-1))
+
+
+def verify(named_tensors, expected: bytes, chunk_bytes: int) -> None:
+    """Raise VerificationError unless the manifest root of the tensors equals ``expected``."""
+    items = sorted(named_tensors.items(), key=lambda kv: kv[0].encode("utf-8")) \
+        if isinstance(named_tensors, dict) else list(named_tensors)
+    v = Verifier(items[0][1].device)
+    root = v.manifest_root([t for _, t in items], chunk_bytes)
+    if not v.verify_root(root, expected):
+        raise VerificationError("model root does not match the expected root")

@@ -1,0 +1,142 @@
+"""The C-ABI library loads, exports what include/hv.h declares, and its
+host-side planning and argument checks behave as documented.
+
+These run without a GPU: every call here either is host-only (hv_leaf_layout,
+the *_workspace_bytes sizers, hv_last_error) or fails validation before the
+library issues any HIP call.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from conftest import ROOT
+from oracle import oracle
+
+hv = pytest.importorskip("paper_2510_23938_amd.hv")
+
+
+def declared_functions():
+    import glob
+
+    text = "".join(open(f).read() for f in sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))))
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hv_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 12
+    lib = ctypes.CDLL(hv.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(hv.EXPORTS) == names
+
+
+def test_kernel_round_constants_match_their_definition():
+    # the HIP source's own tables, re-derived from primes (FIPS 180-4 4.2.2, 5.3.3)
+    from test_oracle_sha256 import first_primes, iroot
+
+    src = open(os.path.join(ROOT, "paper_2510_23938_amd", "csrc", "sha256_device.h")).read()
+    k_body = re.search(r"kRound\[64\]\s*=\s*\{(.*?)\};", src, re.S).group(1)
+    h_body = re.search(r"kInit\[8\]\s*=\s*\{(.*?)\};", src, re.S).group(1)
+    K = [int(x, 16) for x in re.findall(r"0x([0-9a-fA-F]+)u", k_body)]
+    H = [int(x, 16) for x in re.findall(r"0x([0-9a-fA-F]+)u", h_body)]
+    p = first_primes(64)
+    assert K == [iroot(q << 96, 3) & 0xFFFFFFFF for q in p]
+    assert H == [iroot(q << 64, 2) & 0xFFFFFFFF for q in p[:8]]
+
+
+def _msgs(lens, base=0x10000):
+    ptrs = np.array([base + 4096 * i if n else 0 for i, n in enumerate(lens)], dtype=np.uint64)
+    return ptrs, np.array(lens, dtype=np.uint64)
+
+
+@pytest.mark.parametrize("C", [64, 128, 4096, 1 << 20, 0])
+def test_leaf_layout_matches_oracle_chunk_count(C):
+    lens = [0, 1, 63, 64, 65, 4095, 4096, 4097, 3 * 4096, (1 << 20) + 5, 12345678]
+    seg, n = hv.hv_leaf_layout(*_msgs(lens), C)
+    counts = [oracle.chunk_count(x, C) for x in lens]
+    assert n == sum(counts)
+    assert list(seg) == list(np.concatenate([[0], np.cumsum(counts)]))
+
+
+@pytest.mark.parametrize("C", [1, 32, 100, 65])
+def test_bad_chunk_size_rejected(C):
+    with pytest.raises(hv.HVError) as e:
+        hv.hv_leaf_layout(*_msgs([100]), C)
+    assert e.value.status == hv.HV_ERR_INVALID_ARG
+    assert "multiple of 64" in str(e.value)
+
+
+def test_null_data_with_bytes_rejected():
+    ptrs = np.array([0x1000, 0], dtype=np.uint64)
+    lens = np.array([10, 5], dtype=np.uint64)
+    with pytest.raises(hv.HVError) as e:
+        hv.hv_leaf_layout(ptrs, lens, 64)
+    assert e.value.status == hv.HV_ERR_INVALID_ARG and "message 1" in str(e.value)
+
+
+def test_null_n_leaves_and_msgs_rejected():
+    assert hv.lib.hv_leaf_layout(None, 3, 64, None, None) == hv.HV_ERR_INVALID_ARG
+    n = ctypes.c_uint64(0)
+    assert hv.lib.hv_leaf_layout(None, 3, 64, None, ctypes.byref(n)) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_leaf_layout(None, 0, 64, None, ctypes.byref(n)) == hv.HV_OK and n.value == 0
+
+
+def test_workspace_sizes_grow_and_are_aligned():
+    a = hv.lib.hv_hash_workspace_bytes(10, 100)
+    b = hv.lib.hv_hash_workspace_bytes(10, 100000)
+    assert b > a and a % 256 == 0 and b % 256 == 0
+    assert hv.lib.hv_hash_workspace_bytes(1_000_000, 1_000_000) >= 1_000_000 * (16 + 24)
+    m1 = hv.lib.hv_merkle_workspace_bytes(1000, 1)
+    m2 = hv.lib.hv_merkle_workspace_bytes(10_000_000, 723)
+    assert m2 > m1 and m1 % 256 == 0
+    assert hv.lib.hv_verify_workspace_bytes() >= 4
+
+
+def test_hash_rejects_before_launch():
+    # every one of these fails validation before any HIP call
+    ptrs, lens = _msgs([1000, 64])
+    arr = hv._msg_array(ptrs, lens)
+    p = arr.ctypes.data
+    st = hv.lib.hv_hash_chunks(p, 2, 100, 0x1000, 0x100000, 1 << 30, None)
+    assert st == hv.HV_ERR_INVALID_ARG
+    st = hv.lib.hv_hash_chunks(p, 2, 64, None, 0x100000, 1 << 30, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"leaf_digests" in hv.lib.hv_last_error()
+    st = hv.lib.hv_hash_chunks(p, 2, 64, 0x1008, 0x100000, 1 << 30, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"aligned" in hv.lib.hv_last_error()
+    st = hv.lib.hv_hash_chunks(p, 2, 64, 0x1000, 0x100000, 16, None)
+    assert st == hv.HV_ERR_WORKSPACE
+    st = hv.lib.hv_hash_chunks(p, 2, 64, 0x1000, None, 1 << 30, None)
+    assert st == hv.HV_ERR_WORKSPACE
+
+
+def test_merkle_rejects_before_launch():
+    seg = np.array([0, 5, 3], dtype=np.uint64)  # decreasing
+    st = hv.lib.hv_merkle_reduce(0x1000, seg.ctypes.data, 2, 0x2000, 0x100000, 1 << 20, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"decreases" in hv.lib.hv_last_error()
+    seg = np.array([1, 5], dtype=np.uint64)
+    assert hv.lib.hv_merkle_reduce(0x1000, seg.ctypes.data, 1, 0x2000, 0x100000, 1 << 20, None) == \
+        hv.HV_ERR_INVALID_ARG
+    seg = np.array([0, 5], dtype=np.uint64)
+    assert hv.lib.hv_merkle_reduce(0x1000, seg.ctypes.data, 0, 0x2000, 0x100000, 1 << 20, None) == \
+        hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_merkle_reduce(None, seg.ctypes.data, 1, 0x2000, 0x100000, 1 << 20, None) == \
+        hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_merkle_reduce(0x1000, seg.ctypes.data, 1, 0x2000, 0x100000, 8, None) == hv.HV_ERR_WORKSPACE
+
+
+def test_verify_rejects_before_launch():
+    exp = (ctypes.c_uint8 * 32)()
+    m = ctypes.c_int(0)
+    assert hv.lib.hv_verify_root(None, exp, ctypes.byref(m), 0x1000, 256, None) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_verify_root(0x1000, exp, ctypes.byref(m), None, 256, None) == hv.HV_ERR_WORKSPACE
+    assert hv.lib.hv_compare_roots(None, None, 3, None, None) == hv.HV_ERR_INVALID_ARG
+
+
+def test_timing_query_without_timed_call():
+    with pytest.raises(hv.HVError):
+        hv.leaf_kernel_ms()

@@ -1,0 +1,139 @@
+"""GPU path vs the CPU oracle, bit for bit, at sizes the oracle finishes in seconds.
+
+Every call goes through the C ABI (libhv.so) via the ctypes binding.  Inputs
+come from the seeded generators in ``workloads``; expected values come only
+from ``oracle``.
+"""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import oracle
+
+hv = pytest.importorskip("paper_2510_23938_amd.hv")
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda")
+
+
+def place(lens, align_off, seed, gap=16):
+    """One device buffer holding the messages at 16-byte slots + align_off.
+
+    Returns (buf, host bytes, ptrs, lens, starts)."""
+    lens = np.asarray(lens, dtype=np.uint64)
+    starts = np.zeros(len(lens), dtype=np.uint64)
+    pos = 0
+    for i, n in enumerate(lens):
+        starts[i] = pos + align_off
+        pos += (int(n) + align_off + gap + 15) // 16 * 16
+    buf = W.random_bytes(max(pos, 1), seed, DEV)
+    host = buf.cpu().numpy()
+    ptrs = np.uint64(buf.data_ptr()) + starts
+    ptrs[lens == 0] = 0  # empty messages may carry a NULL pointer
+    return buf, host, ptrs, lens, starts
+
+
+def host_msgs(host, starts, lens):
+    return [host[int(s):int(s) + int(n)] for s, n in zip(starts, lens)]
+
+
+def check_all(buf, host, ptrs, lens, starts, C, tag=""):
+    v = hv.Verifier(DEV)
+    leaves, seg = v.leaf_digests((ptrs, lens), C)
+    roots = hv.hv_merkle_reduce(leaves, seg, v.ws_tree)
+    manifest = hv.hv_merkle_reduce(roots, np.array([0, len(lens)], dtype=np.uint64), v.ws_manifest)
+    torch.cuda.synchronize()
+    msgs = host_msgs(host, starts, lens)
+    want_leaves = oracle.leaf_digests_mt(msgs, C, 8)
+    got_leaves = leaves.cpu().numpy()
+    if not np.array_equal(got_leaves, want_leaves):
+        bad = np.nonzero((got_leaves != want_leaves).any(axis=1))[0]
+        owner = np.searchsorted(seg, bad[0], side="right") - 1
+        raise AssertionError(f"{tag}: {len(bad)} leaf digests differ; first leaf {bad[0]} "
+                             f"(message {owner}, length {int(lens[owner])}, C={C})")
+    counts = np.diff(seg)
+    want_roots = oracle.seg_roots_from_leaves(want_leaves, counts)
+    got_roots = [bytes(r) for r in roots.cpu().numpy()]
+    assert got_roots == want_roots, f"{tag}: segment roots differ"
+    assert bytes(manifest.cpu().numpy().reshape(-1)) == oracle.mth(want_roots), f"{tag}: manifest differs"
+    return want_roots
+
+
+@pytest.mark.parametrize("align_off", [0, 1, 3, 15])
+@pytest.mark.parametrize("C", [64, 128, 4096, 0])
+def test_every_length_up_to_4160(C, align_off):
+    lens = np.arange(0, 4161)
+    buf, host, ptrs, lens, starts = place(lens, align_off, seed=100 + align_off)
+    check_all(buf, host, ptrs, lens, starts, C, f"C={C} off={align_off}")
+
+
+@pytest.mark.parametrize("C", [64, 4096, 65536, 1 << 20, 0])
+def test_mixed_batch(C):
+    rng = np.random.default_rng(7)
+    lens = np.concatenate([
+        rng.integers(0, 300, 200), rng.integers(1, 70000, 200), [0, 0, 1, 64, 65536, 65537, 3 * (1 << 20) + 11],
+        rng.integers(1 << 20, 3 << 20, 4),
+    ])
+    rng.shuffle(lens)
+    buf, host, ptrs, lens, starts = place(lens, 0, seed=8)
+    check_all(buf, host, ptrs, lens, starts, C, f"mixed C={C}")
+
+
+def test_bf16_tensors_as_messages():
+    named = [(f"t{i}", W.bf16_weights(s, 50 + i, DEV)) for i, s in enumerate([(3, 7), (1000, 33), (2048,), (64, 1024)])]
+    C = 4096
+    v = hv.Verifier(DEV)
+    roots, leaves, seg = v.roots([t for _, t in named], C)
+    torch.cuda.synchronize()
+    host = [W.as_bytes(t).cpu().numpy().tobytes() for _, t in named]
+    assert [bytes(r) for r in roots.cpu().numpy()] == [oracle.seg_root(m, C) for m in host]
+    assert hv.manifest_root(dict(named), C) == oracle.manifest_root([host[i] for i in (0, 1, 2, 3)], C)
+
+
+def test_empty_cases():
+    v = hv.Verifier(DEV)
+    # no messages at all
+    leaves, seg = v.leaf_digests((np.zeros(0, np.uint64), np.zeros(0, np.uint64)), 64)
+    assert leaves.shape == (0, 32) and list(seg) == [0]
+    # empty messages: no leaves with C > 0, one leaf each with C = 0
+    ptrs, lens = np.zeros(3, np.uint64), np.zeros(3, np.uint64)
+    leaves, seg = v.leaf_digests((ptrs, lens), 64)
+    assert leaves.shape == (0, 32)
+    roots = hv.hv_merkle_reduce(leaves, seg, v.ws_tree)
+    assert [bytes(r) for r in roots.cpu().numpy()] == [oracle.mth([])] * 3
+    leaves, seg = v.leaf_digests((ptrs, lens), 0)
+    assert [bytes(r) for r in leaves.cpu().numpy()] == [oracle.sha256(b"")] * 3
+
+
+@pytest.mark.parametrize("sizes", [
+    [0], [1], [2], [3], [5], [511, 512, 513], [0, 1, 0, 2, 0], [1023, 1024, 1025, 4097],
+    [300_000], [262_145, 3, 0, 70_000],
+])
+def test_merkle_segments(sizes):
+    n = int(sum(sizes))
+    entries = W.random_bytes(max(n, 1) * 32, 200 + n, DEV)[: n * 32].view(n, 32)
+    seg = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    roots = hv.hv_merkle_reduce(entries, seg)
+    torch.cuda.synchronize()
+    host = entries.cpu().numpy()
+    want = [oracle.mth(host[int(seg[s]):int(seg[s + 1])]) for s in range(len(sizes))]
+    assert [bytes(r) for r in roots.cpu().numpy()] == want
+
+
+def test_verify_and_compare():
+    entries = W.random_bytes(5 * 32, 300, DEV).view(5, 32)
+    root = hv.hv_merkle_reduce(entries, np.array([0, 5], dtype=np.uint64))
+    want = oracle.mth(entries.cpu().numpy())
+    assert hv.hv_verify_root(root, want)
+    for byte in (0, 13, 31):
+        for bit in (0, 7):
+            bad = bytearray(want)
+            bad[byte] ^= 1 << bit
+            assert not hv.hv_verify_root(root, bytes(bad))
+    a = W.random_bytes(10 * 32, 301, DEV).view(10, 32)
+    b = a.clone()
+    b[3, 0] ^= 1
+    b[9, 31] ^= 128
+    mism = hv.hv_compare_roots(a, b).cpu().numpy()
+    assert list(np.nonzero(mism)[0]) == [3, 9]
