@@ -40,6 +40,7 @@ EXPORTS = (
     "hv_merkle_reduce", "hv_verify_workspace_bytes", "hv_verify_root", "hv_compare_roots",
     "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
     "hv_leaf_schedule",  # include/hv_inspect.h
+    "hv_mb_valu", "hv_mb_hbm_read",  # include/hv_microbench.h
 )
 
 
@@ -77,6 +78,8 @@ def _load():
         "hv_set_kernel_timing": ([ctypes.c_int], ctypes.c_int),
         "hv_leaf_kernel_ms": ([vp], ctypes.c_int),
         "hv_leaf_schedule": ([vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
+        "hv_mb_valu": ([vp, u32, u32, vp, vp], ctypes.c_int),
+        "hv_mb_hbm_read": ([vp, u64, vp, u32, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -209,6 +212,47 @@ def hv_leaf_schedule(msgs, chunk_bytes: int, device="cuda") -> np.ndarray:
     return table
 
 
+def measure_valu_peak(device="cuda", grid=16384, iters=4096, reps=5) -> dict:
+    """Best rate of the SHA-256 VALU mix (alignbit / bitop3 / add3) over reps launches."""
+    dev = torch.device(device)
+    sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
+    ops = ctypes.c_uint64(0)
+    s = _stream(dev)
+    _check(lib.hv_mb_valu(sink.data_ptr(), grid, 64, ctypes.byref(ops), s))  # warm-up
+    best = None
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        _check(lib.hv_mb_valu(sink.data_ptr(), grid, iters, ctypes.byref(ops), s))
+        b.record()
+        b.synchronize()
+        ms = a.elapsed_time(b)
+        best = ms if best is None else min(best, ms)
+    return {"tops": ops.value / (best / 1e3) / 1e12, "ms": best, "ops": ops.value, "grid": grid, "iters": iters}
+
+
+def measure_hbm_read(nbytes=16 << 30, device="cuda", grid=None, reps=5) -> dict:
+    """Best streaming-read bandwidth over reps launches on an nbytes buffer."""
+    dev = torch.device(device)
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    buf.fill_(1)
+    grid = grid or 256 * 64
+    sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
+    s = _stream(dev)
+    _check(lib.hv_mb_hbm_read(buf.data_ptr(), nbytes, sink.data_ptr(), grid, s))
+    best = None
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        _check(lib.hv_mb_hbm_read(buf.data_ptr(), nbytes, sink.data_ptr(), grid, s))
+        b.record()
+        b.synchronize()
+        ms = a.elapsed_time(b)
+        best = ms if best is None else min(best, ms)
+    del buf
+    return {"GBps": nbytes / (best / 1e3) / 1e9, "ms": best, "bytes": nbytes, "grid": grid}
+
+
 def set_kernel_timing(enable: bool):
     _check(lib.hv_set_kernel_timing(1 if enable else 0))
 
@@ -249,6 +293,71 @@ class Verifier:
 
     def verify_root(self, root: torch.Tensor, expected: bytes) -> bool:
         return hv_verify_root(root.reshape(-1)[:32], expected, self.ws_verify)
+
+
+class Pipeline:
+    """One message set, marshalled once, run many times: the whole path.
+
+    mode "manifest": chunk digests -> one root per message -> one root over
+    those (hierarchical roots); mode "single": chunk digests -> one root over
+    all of them.  ``run(expected)`` ends with the on-GPU root comparison and
+    returns its verdict.  Outputs and workspaces are allocated here, once.
+    """
+
+    def __init__(self, msgs, chunk_bytes: int, mode: str = "manifest", device="cuda"):
+        if mode not in ("manifest", "single"):
+            raise ValueError(mode)
+        self.device = torch.device(device)
+        self.mode, self.C = mode, int(chunk_bytes)
+        ptrs, lens = _ptr_len(msgs)
+        self.keepalive = msgs
+        self.arr = _msg_array(ptrs, lens)
+        self.n_msgs = len(self.arr)
+        self.seg, self.n_leaves = hv_leaf_layout(ptrs, lens, self.C)
+        self.total_bytes = int(np.asarray(lens, dtype=np.uint64).sum()) if self.n_msgs else 0
+        self.leaves = torch.empty((self.n_leaves, 32), dtype=torch.uint8, device=self.device)
+        self.ws_hash = Workspace(self.device).get(lib.hv_hash_workspace_bytes(self.n_msgs, self.n_leaves))
+        if mode == "manifest":
+            self.tree_seg = self.seg
+            self.roots = torch.empty((self.n_msgs, 32), dtype=torch.uint8, device=self.device)
+            self.top_seg = np.array([0, self.n_msgs], dtype=np.uint64)
+            self.ws_top = Workspace(self.device).get(lib.hv_merkle_workspace_bytes(self.n_msgs, 1))
+        else:
+            self.tree_seg = np.array([0, self.n_leaves], dtype=np.uint64)
+            self.roots = torch.empty((1, 32), dtype=torch.uint8, device=self.device)
+        self.ws_tree = Workspace(self.device).get(
+            lib.hv_merkle_workspace_bytes(int(self.tree_seg[-1]), len(self.tree_seg) - 1))
+        self.root = torch.empty((1, 32), dtype=torch.uint8, device=self.device)
+        self.ws_verify = Workspace(self.device).get(lib.hv_verify_workspace_bytes())
+
+    def compute(self):
+        """Queue the digests and roots on the current stream; returns the [1, 32] root."""
+        s = _stream(self.device)
+        _check(lib.hv_hash_chunks(self.arr.ctypes.data if self.n_msgs else None, self.n_msgs, self.C,
+                                  self.leaves.data_ptr() if self.n_leaves else None,
+                                  self.ws_hash.data_ptr(), self.ws_hash.numel(), s))
+        _check(lib.hv_merkle_reduce(self.leaves.data_ptr() if self.n_leaves else None, self.tree_seg.ctypes.data,
+                                    len(self.tree_seg) - 1, self.roots.data_ptr(),
+                                    self.ws_tree.data_ptr(), self.ws_tree.numel(), s))
+        if self.mode == "single":
+            return self.roots
+        _check(lib.hv_merkle_reduce(self.roots.data_ptr() if self.n_msgs else None, self.top_seg.ctypes.data, 1,
+                                    self.root.data_ptr(), self.ws_top.data_ptr(), self.ws_top.numel(), s))
+        return self.root
+
+    def run(self, expected: bytes) -> bool:
+        """The whole path: digests, roots, comparison with ``expected`` (synchronous)."""
+        root = self.compute()
+        return hv_verify_root(root, expected, _FixedWorkspace(self.ws_verify))
+
+
+class _FixedWorkspace:
+    def __init__(self, buf):
+        self.buf = buf
+
+    def get(self, nbytes):
+        assert self.buf.numel() >= nbytes
+        return self.buf
 
 
 def manifest_root(named_tensors, chunk_bytes: int) -> bytes:
