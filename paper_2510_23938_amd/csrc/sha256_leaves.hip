@@ -8,32 +8,115 @@
 // blocks first, then one or two final blocks holding the 0..63 tail bytes,
 // the 0x80 byte, zeros and the 64-bit bit length.
 //
-// Memory safety at tails: every load is a dword (or wider, 16-byte aligned)
-// access that contains at least one byte of the chunk, so no access touches a
-// page the chunk does not touch.  Bytes past the chunk end that such a load
-// brings in are masked off before hashing.
+// Load path for whole blocks (16-byte aligned chunks, the usual case): the
+// wave stages its 64 chunks through LDS, 128 bytes (two blocks, one HBM line)
+// per chunk per stage, with direct-to-LDS 16-byte loads
+// (global_load_lds_dwordx4).  Load instruction j of a stage covers chunks
+// 8j..8j+7, eight lanes per chunk, so every instruction reads eight whole
+// 128-byte lines and every line is read from HBM once.  The 16-byte slots of
+// a chunk's row are XOR-swizzled by chunk index so that the 64 lanes reading
+// their own rows with ds_read_b128 hit distinct banks.  A stage is copied to
+// VGPRs before the next stage's loads are issued into the same buffer, so
+// the loads run under the two compressions of the current stage.  Chunks
+// that are not 16-byte aligned take a dword-gather path instead.
+//
+// Memory safety at tails: the final partial block is read with aligned dword
+// loads that each contain at least one byte of the chunk, so no access
+// touches a page the chunk does not touch; bytes past the end are masked off.
 #include "hv_kernels.h"
 #include "sha256_device.h"
 
 namespace hv {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;                     // four waves per workgroup
+constexpr int kWaves = kThreads / 64;
+constexpr int kStageBytes = 128;                  // bytes per chunk per stage
+constexpr int kRowsPerLoad = 1024 / kStageBytes;  // chunks covered by one 64-lane 16-byte load
 
-// Whole blocks from a 16-byte aligned chunk: four 16-byte loads per block,
-// issued one block ahead of the compression that consumes them.
-__device__ __forceinline__ void full_blocks_aligned(uint32_t H[8], const uint8_t* p, uint64_t nfull) {
-    if (nfull == 0) return;
-    const uint4* q = reinterpret_cast<const uint4*>(p);
-    uint4 x0 = q[0], x1 = q[1], x2 = q[2], x3 = q[3];
-    for (uint64_t b = 0; b < nfull; ++b) {
-        uint32_t W[16] = {bswap(x0.x), bswap(x0.y), bswap(x0.z), bswap(x0.w), bswap(x1.x), bswap(x1.y),
-                          bswap(x1.z), bswap(x1.w), bswap(x2.x), bswap(x2.y), bswap(x2.z), bswap(x2.w),
-                          bswap(x3.x), bswap(x3.y), bswap(x3.z), bswap(x3.w)};
-        // next block, or the current one again on the last iteration (in range)
-        const uint64_t nb = b + 1 < nfull ? b + 1 : b;
-        x0 = q[4 * nb]; x1 = q[4 * nb + 1]; x2 = q[4 * nb + 2]; x3 = q[4 * nb + 3];
-        compress(H, W);
+// Swizzle of a chunk's 16-byte slots within its LDS row.  Consecutive lanes
+// (rows) differ in (c ^ c>>3) & 7, so the eight slots a group of lanes reads
+// at once fall in different banks whether the LDS serves 8 or 16 lanes of a
+// 16-byte read per cycle.
+__device__ __forceinline__ uint32_t swizzle(uint32_t c) { return (c ^ (c >> 3)) & 7u; }
+
+__device__ __forceinline__ void words_from(const uint4& x0, const uint4& x1, const uint4& x2, const uint4& x3,
+                                           uint32_t W[16]) {
+    W[0] = bswap(x0.x); W[1] = bswap(x0.y); W[2] = bswap(x0.z); W[3] = bswap(x0.w);
+    W[4] = bswap(x1.x); W[5] = bswap(x1.y); W[6] = bswap(x1.z); W[7] = bswap(x1.w);
+    W[8] = bswap(x2.x); W[9] = bswap(x2.y); W[10] = bswap(x2.z); W[11] = bswap(x2.w);
+    W[12] = bswap(x3.x); W[13] = bswap(x3.y); W[14] = bswap(x3.z); W[15] = bswap(x3.w);
+}
+
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
+__device__ __forceinline__ void wait_lgkm_all() { __builtin_amdgcn_s_waitcnt(0xC07F); }  // lgkmcnt(0)
+
+// Whole blocks of the wave's 64 chunks (every lane's chunk 16-byte aligned),
+// staged through this wave's 8 KB LDS row buffer.  nfull: this lane's whole
+// blocks (< 2^32: a chunk this long would not fit in HBM).
+__device__ __forceinline__ void full_blocks_lds(uint32_t H[8], uint64_t src, uint32_t nfull, uint8_t* rows) {
+    const uint32_t lane = threadIdx.x & 63;
+    uint32_t nmax = nfull, nmin = nfull;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t a = __shfl_xor(nmax, o), b = __shfl_xor(nmin, o);
+        nmax = a > nmax ? a : nmax;
+        nmin = b < nmin ? b : nmin;
+    }
+    nmax = __builtin_amdgcn_readfirstlane(nmax);
+    nmin = __builtin_amdgcn_readfirstlane(nmin);
+    const uint32_t stages = (nmax + 1) / 2;
+    if (stages == 0) return;
+
+    // The 16 bytes this lane moves for load j of every stage: chunk 8j + lane/8,
+    // source slot (lane % 8) ^ swizzle(chunk), landing in LDS slot lane % 8.
+    const uint8_t* from[kRowsPerLoad];
+    uint32_t until[kRowsPerLoad];  // stages in which that slot lies in a whole block
+#pragma unroll
+    for (int j = 0; j < kRowsPerLoad; ++j) {
+        const uint32_t c = kRowsPerLoad * j + (lane >> 3);
+        const uint32_t slot = (lane & 7) ^ swizzle(c);
+        const uint64_t s = __shfl(src, (int)c);
+        const uint32_t nf = __shfl(nfull, (int)c);
+        from[j] = reinterpret_cast<const uint8_t*>(s) + 16 * slot;
+        until[j] = slot < 4 ? (nf + 1) / 2 : nf / 2;
+    }
+    const bool uniform = nmin == nmax;
+
+#pragma unroll
+    for (int j = 0; j < kRowsPerLoad; ++j)
+        if (0 < until[j]) __builtin_amdgcn_global_load_lds(from[j], rows + 1024 * j, 16, 0, 0);
+
+    const uint8_t* row = rows + kStageBytes * lane;
+    const uint32_t sw = swizzle(lane);
+    for (uint32_t st = 0; st < stages; ++st) {
+        wait_vm_all();  // stage st is in LDS
+        uint4 r[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) r[k] = *reinterpret_cast<const uint4*>(row + 16 * (k ^ sw));
+        wait_lgkm_all();  // and in VGPRs: the buffer may be refilled
+        const uint32_t nx = st + 1;
+        if (nx < stages) {
+            const uint32_t off = kStageBytes * nx;
+            if (uniform && 2 * nx + 1 < nmax) {  // whole stage valid for every chunk
+#pragma unroll
+                for (int j = 0; j < kRowsPerLoad; ++j)
+                    __builtin_amdgcn_global_load_lds(from[j] + off, rows + 1024 * j, 16, 0, 0);
+            } else {
+#pragma unroll
+                for (int j = 0; j < kRowsPerLoad; ++j)
+                    if (nx < until[j]) __builtin_amdgcn_global_load_lds(from[j] + off, rows + 1024 * j, 16, 0, 0);
+            }
+        }
+        uint32_t W[16];
+        if (2 * st < nfull) {
+            words_from(r[0], r[1], r[2], r[3], W);
+            compress(H, W);
+        }
+        if (2 * st + 1 < nfull) {
+            words_from(r[4], r[5], r[6], r[7], W);
+            compress(H, W);
+        }
     }
 }
 
@@ -52,10 +135,10 @@ __device__ __forceinline__ void gather_words(const uint8_t* p, uint32_t valid, u
 }
 
 // Whole blocks from a chunk at any alignment.
-__device__ __forceinline__ void full_blocks_any(uint32_t H[8], const uint8_t* p, uint64_t nfull) {
-    for (uint64_t b = 0; b < nfull; ++b) {
+__device__ __forceinline__ void full_blocks_any(uint32_t H[8], const uint8_t* p, uint32_t nfull) {
+    for (uint32_t b = 0; b < nfull; ++b) {
         uint32_t W[16];
-        gather_words(p + 64 * b, 64, W);
+        gather_words(p + 64 * (uint64_t)b, 64, W);
 #pragma unroll
         for (int i = 0; i < 16; ++i) W[i] = bswap(W[i]);
         compress(H, W);
@@ -91,21 +174,23 @@ __device__ __forceinline__ void final_blocks(uint32_t H[8], const uint8_t* p, ui
 
 __global__ void __launch_bounds__(kThreads) sha256_leaves_kernel(const LeafDesc* __restrict__ desc, uint64_t n_leaves,
                                                                  uint8_t* __restrict__ digests) {
+    __shared__ __attribute__((aligned(16))) uint8_t stage[kWaves][64 * kStageBytes];
     const uint64_t slot = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
     const bool live = slot < n_leaves;
     LeafDesc d = {0, 0, 0};
     if (live) d = desc[slot];
     const uint8_t* p = reinterpret_cast<const uint8_t*>(d.src);
-    const uint64_t nfull = d.nbytes >> 6;
+    const uint32_t nfull = (uint32_t)(d.nbytes >> 6);
 
     uint32_t H[8];
     init_state(H);
     if (__all((d.src & 15) == 0)) {
-        full_blocks_aligned(H, p, nfull);
+        const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        full_blocks_lds(H, d.src, nfull, stage[wave]);
     } else {
         full_blocks_any(H, p, nfull);
     }
-    final_blocks(H, p + (nfull << 6), (uint32_t)(d.nbytes & 63), d.nbytes);
+    final_blocks(H, p + ((uint64_t)nfull << 6), (uint32_t)(d.nbytes & 63), d.nbytes);
     if (live && d.out < n_leaves) store_digest(digests + 32 * d.out, H);
 }
 
