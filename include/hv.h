@@ -71,8 +71,11 @@ enum { HV_DIGEST_BYTES = 32 };
  *   seg_offsets: optional (may be NULL), n_msgs + 1 entries: seg_offsets[0] = 0,
  *                seg_offsets[m+1] - seg_offsets[m] = leaves of message m.
  *   n_leaves:    required, total leaves.
+ * A single chunk may hold at most 2^38 - 64 bytes (256 GiB, more than one
+ * GPU's memory).
  * Errors: HV_ERR_INVALID_ARG for msgs == NULL with n_msgs > 0, a NULL data
- * pointer with nbytes > 0, a bad C, a NULL n_leaves, or a count overflow. */
+ * pointer with nbytes > 0, a bad C, a chunk over the size limit, a NULL
+ * n_leaves, or a count overflow. */
 hv_status hv_leaf_layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
                          uint64_t* seg_offsets, uint64_t* n_leaves);
 
@@ -86,7 +89,8 @@ size_t hv_hash_workspace_bytes(uint32_t n_msgs, uint64_t n_leaves);
  *   msgs:         host array of n_msgs device messages (read during the call;
  *                 the descriptors are copied to the workspace).
  *   chunk_bytes:  0 or a multiple of 64.
- *   leaf_digests: device, n_leaves * 32 bytes, caller-owned, written.
+ *   leaf_digests: device, n_leaves * 32 bytes, 16-byte aligned, caller-owned,
+ *                 written.
  *   workspace:    device, >= hv_hash_workspace_bytes(n_msgs, n_leaves) bytes,
  *                 256-byte aligned; contents are scratch.
  * Errors: as hv_leaf_layout, plus leaf_digests == NULL with n_leaves > 0,
@@ -106,12 +110,15 @@ size_t hv_merkle_workspace_bytes(uint64_t n_nodes, uint32_t n_seg);
  * MTH(D[0:n]) = SHA-256(0x01 || MTH(D[0:k]) || MTH(D[k:n])), k the largest
  * power of two below n.  Entries are 32-byte values (chunk digests, or
  * segment roots for a manifest over tensors -- the hierarchical roots).
- *   nodes:       device, seg_offsets[n_seg] * 32 bytes, read only.
+ *   nodes:       device, seg_offsets[n_seg] * 32 bytes, 16-byte aligned, read only.
  *   seg_offsets: host, n_seg + 1 entries, seg_offsets[0] == 0, non-decreasing.
- *   roots:       device, n_seg * 32 bytes, written.
+ *   roots:       device, n_seg * 32 bytes, 16-byte aligned, written.
  *   workspace:   device, >= hv_merkle_workspace_bytes(seg_offsets[n_seg], n_seg).
- * Errors: HV_ERR_INVALID_ARG for n_seg == 0, NULL pointers, offsets that do
- * not start at 0 or decrease; HV_ERR_WORKSPACE; HV_ERR_HIP. */
+ * The host plans ceil(depth / 9) launches from seg_offsets and uploads that
+ * plan (a copy from pageable memory, so the call returns once the stream has
+ * reached it).
+ * Errors: HV_ERR_INVALID_ARG for n_seg == 0, NULL or misaligned pointers,
+ * offsets that do not start at 0 or decrease; HV_ERR_WORKSPACE; HV_ERR_HIP. */
 hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg,
                            uint8_t* roots, void* workspace, size_t workspace_bytes,
                            hipStream_t stream);

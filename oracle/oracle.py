@@ -57,8 +57,7 @@ def _load():
     lib.oracle_seg_root.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_void_p]
     lib.oracle_seg_root.restype = None
     lib.oracle_leaf_digests_mt.argtypes = [
-        ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_uint64), ctypes.c_uint32,
-        ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int,
     ]
     lib.oracle_leaf_digests_mt.restype = ctypes.c_uint64
     _lib = lib
@@ -148,12 +147,32 @@ def verify(root: bytes, expected: bytes) -> bool:
 def leaf_digests_mt(messages, C: int, nthreads: int) -> np.ndarray:
     """[n_leaves, 32]: chunk digests of all messages (message-major), on nthreads threads."""
     arrs = [_as_u8(m) for m in messages]
-    n = len(arrs)
-    ptrs = (ctypes.c_void_p * max(n, 1))(*[a.ctypes.data if a.size else None for a in arrs])
-    lens = (ctypes.c_uint64 * max(n, 1))(*[a.size for a in arrs])
-    total = sum(chunk_count(a.size, C) for a in arrs)
+    ptrs = np.array([a.ctypes.data if a.size else 0 for a in arrs], dtype=np.uint64)
+    lens = np.array([a.size for a in arrs], dtype=np.uint64)
+    return _leaf_digests_raw(ptrs, lens, C, nthreads)
+
+
+def leaf_digests_mt_packed(buf: np.ndarray, offsets, lens, C: int, nthreads: int) -> np.ndarray:
+    """As leaf_digests_mt for messages lying in one host buffer at byte offsets."""
+    b = _as_u8(buf)
+    offsets = np.asarray(offsets, dtype=np.uint64)
+    lens = np.asarray(lens, dtype=np.uint64)
+    if len(lens) and int((offsets + lens).max()) > b.size:
+        raise ValueError("message range outside the buffer")
+    ptrs = np.uint64(b.ctypes.data) + offsets
+    return _leaf_digests_raw(ptrs, lens, C, nthreads)
+
+
+def _leaf_digests_raw(ptrs: np.ndarray, lens: np.ndarray, C: int, nthreads: int) -> np.ndarray:
+    n = len(lens)
+    if C != 0:
+        chunk_count(0, C)  # validates C
+        total = int(np.sum(lens // np.uint64(C) + (lens % np.uint64(C) != 0))) if n else 0
+    else:
+        total = n
     out = np.zeros((total, 32), dtype=np.uint8)
-    got = _load().oracle_leaf_digests_mt(ptrs, lens, n, C, out.ctypes.data if total else None, nthreads)
+    got = _load().oracle_leaf_digests_mt(ptrs.ctypes.data if n else None, lens.ctypes.data if n else None, n, C,
+                                         out.ctypes.data if total else None, nthreads)
     if got != total:
         raise RuntimeError("oracle_leaf_digests_mt failed")
     return out

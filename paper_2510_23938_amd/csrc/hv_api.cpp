@@ -35,6 +35,8 @@ size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 // Largest leaf count one call accepts: the hash grid is 256 lanes per block
 // in a 32-bit block index.
 constexpr uint64_t kMaxLeaves = (uint64_t)1 << 38;
+// Largest chunk: the leaf kernel counts a chunk's 64-byte blocks in 32 bits.
+constexpr uint64_t kMaxChunkBytes = ((uint64_t)1 << 38) - 64;
 
 // Carves consecutive 256-byte-aligned regions out of a workspace.
 struct Carver {
@@ -86,6 +88,10 @@ hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_
             return fail(HV_ERR_INVALID_ARG, "message %u has NULL data and %llu bytes", m, (unsigned long long)len);
         if ((uintptr_t)msgs[m].data + len < (uintptr_t)msgs[m].data)
             return fail(HV_ERR_INVALID_ARG, "message %u wraps the address space", m);
+        const uint64_t longest = C == 0 || len < C ? len : C;
+        if (longest > kMaxChunkBytes)
+            return fail(HV_ERR_INVALID_ARG, "message %u: a chunk of %llu bytes exceeds the %llu-byte limit", m,
+                        (unsigned long long)longest, (unsigned long long)kMaxChunkBytes);
         uint64_t leaves;
         if (C == 0) {
             leaves = 1;

@@ -79,6 +79,17 @@ def test_null_data_with_bytes_rejected():
     assert e.value.status == hv.HV_ERR_INVALID_ARG and "message 1" in str(e.value)
 
 
+def test_chunk_size_limit():
+    big = (1 << 38) - 64
+    ptrs = np.array([0x1000], dtype=np.uint64)
+    assert hv.hv_leaf_layout(ptrs, np.array([big], dtype=np.uint64), 0)[1] == 1
+    assert hv.hv_leaf_layout(ptrs, np.array([1 << 40], dtype=np.uint64), 1 << 20)[1] == 1 << 20
+    for lens, C in (([big + 64], 0), ([1 << 39], 1 << 38)):
+        with pytest.raises(hv.HVError) as e:
+            hv.hv_leaf_layout(ptrs, np.array(lens, dtype=np.uint64), C)
+        assert e.value.status == hv.HV_ERR_INVALID_ARG and "limit" in str(e.value)
+
+
 def test_null_n_leaves_and_msgs_rejected():
     assert hv.lib.hv_leaf_layout(None, 3, 64, None, None) == hv.HV_ERR_INVALID_ARG
     n = ctypes.c_uint64(0)

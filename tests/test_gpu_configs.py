@@ -1,0 +1,180 @@
+"""The five workloads at their full sizes, in the launch configuration bench.py
+times, against the CPU oracle.
+
+* 64 MiB blob, 1B-shaped and 7B-shaped weight sets, 10^6 small messages:
+  every leaf digest, every root and the top root, bit for bit, against the
+  threaded oracle over a host copy of the same device bytes.
+* 70B-shaped weight set (141 GB): with every byte set to one value, every
+  per-tensor root and the manifest against the oracle's closed form (RFC 6962
+  over constant chunks, memoised); with random bf16 weights, every leaf
+  digest, per-tensor root and the manifest against the threaded oracle,
+  streamed tensor by tensor; then a seeded one-byte flip in the weights (the
+  manifest changes and the per-tensor comparison names exactly the flipped
+  tensor) and a flipped byte of the expected root (verification fails).
+"""
+import gc
+import hashlib
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import oracle
+
+hv = pytest.importorskip("paper_2510_23938_amd.hv")
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda")
+
+
+def threads():
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def free():
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def pipeline(wl):
+    pipe = hv.Pipeline(wl.msgs, wl.chunk_bytes, "manifest" if wl.manifest else "single", DEV)
+    root = bytes(pipe.compute().cpu().numpy().reshape(-1))
+    torch.cuda.synchronize()
+    return pipe, root
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_model_shaped_workloads_in_full(k):
+    wl = W.workload(k, DEV)
+    pipe, root = pipeline(wl)
+    host = [v.cpu().numpy() for v in wl.msgs.views]
+    C = wl.chunk_bytes
+    want = oracle.leaf_digests_mt(host, C, threads())
+    assert np.array_equal(pipe.leaves.cpu().numpy(), want), f"workload {k}: leaf digests differ"
+    counts = [oracle.chunk_count(h.size, C) for h in host]
+    roots = oracle.seg_roots_from_leaves(want, counts)
+    if wl.manifest:
+        assert [bytes(r) for r in pipe.roots.cpu().numpy()] == roots
+        expected = oracle.mth(roots)
+    else:
+        expected = roots[0]
+    assert root == expected
+    assert pipe.run(expected)
+    del wl, pipe, host
+    free()
+
+
+@pytest.mark.timeout(600)
+def test_million_small_messages_in_full():
+    wl = W.workload(4, DEV)
+    pipe, root = pipeline(wl)
+    host = wl.msgs.buffer.cpu().numpy()
+    want = oracle.leaf_digests_mt_packed(host, wl.msgs.offsets, wl.msgs.lens, 0, threads())
+    got = pipe.leaves.cpu().numpy()
+    assert np.array_equal(got, want), f"{int((got != want).any(axis=1).sum())} message digests differ"
+    expected = oracle.mth(want)
+    assert root == expected
+    assert pipe.run(expected)
+    del wl, pipe, host
+    free()
+
+
+def shard_split_root(left: bytes, right: bytes) -> bytes:
+    return hashlib.sha256(b"\x01" + left + right).digest()
+
+
+@pytest.mark.timeout(600)
+def test_70b_constant_bytes_closed_form():
+    value = 0x3C
+    named = []
+    for name, shape in W.tensors_70b():
+        t = torch.empty(W.numel(shape) * 2, dtype=torch.uint8, device=DEV)
+        t.fill_(value)
+        named.append((name, t))
+    ms = W.message_set(named)
+    C = W.CHUNK_BYTES[5]
+    pipe = hv.Pipeline(ms, C, "manifest", DEV)
+    root = bytes(pipe.compute().cpu().numpy().reshape(-1))
+    cache = {}
+    want = []
+    for L in ms.lens:
+        L = int(L)
+        if L not in cache:
+            cache[L] = oracle.const_seg_root(L, C, value)
+        want.append(cache[L])
+    got = [bytes(r) for r in pipe.roots.cpu().numpy()]
+    assert got == want
+    assert root == oracle.mth(want)
+    del named, ms, pipe
+    free()
+
+
+@pytest.fixture(scope="module")
+def w70b():
+    wl = W.workload(5, DEV)
+    pipe, root = pipeline(wl)
+    yield wl, pipe, root
+    del wl, pipe
+    free()
+
+
+@pytest.mark.timeout(900)
+def test_70b_random_weights_full_oracle(w70b):
+    wl, pipe, root = w70b
+    C = wl.chunk_bytes
+    gpu_leaves = pipe.leaves.cpu().numpy()
+    roots = []
+    for m, view in enumerate(wl.msgs.views):
+        host = view.cpu().numpy()
+        want = oracle.leaf_digests_mt([host], C, threads())
+        lo, hi = int(pipe.seg[m]), int(pipe.seg[m + 1])
+        assert np.array_equal(gpu_leaves[lo:hi], want), f"tensor {wl.msgs.names[m]}: leaf digests differ"
+        roots.append(oracle.mth(want))
+    assert [bytes(r) for r in pipe.roots.cpu().numpy()] == roots
+    assert root == oracle.mth(roots)
+
+
+@pytest.mark.timeout(600)
+def test_70b_sharded_roots_recombine(w70b):
+    # split the largest tensor's leaves at power-of-two-aligned indices, reduce
+    # the parts separately, recombine with interior nodes: the one-shot root
+    wl, pipe, _ = w70b
+    m = int(np.argmax(np.diff(pipe.seg)))
+    lo, hi = int(pipe.seg[m]), int(pipe.seg[m + 1])
+    n = hi - lo
+    leaves = pipe.leaves[lo:hi]
+    k = 1 << ((n - 1).bit_length() - 1)
+    parts = hv.hv_merkle_reduce(leaves, np.array([0, k // 2, k, n], dtype=np.uint64)).cpu().numpy()
+    r0, r1, r2 = (bytes(x) for x in parts)
+    whole = bytes(pipe.roots[m].cpu().numpy())
+    assert shard_split_root(shard_split_root(r0, r1), r2) == whole
+
+
+@pytest.mark.timeout(600)
+def test_70b_flipped_byte_is_detected_and_localised(w70b):
+    wl, pipe, root = w70b
+    clean_roots = pipe.roots.clone()
+    rng = np.random.default_rng(W.seed_of(5) + 1)
+    total = int(wl.msgs.lens.sum())
+    pos = int(rng.integers(0, total))
+    mask = int(rng.integers(1, 256))
+    ends = np.cumsum(wl.msgs.lens.astype(np.int64))
+    m = int(np.searchsorted(ends, pos, side="right"))
+    off = pos - (int(ends[m - 1]) if m else 0)
+    view = wl.msgs.views[m]
+    old = int(view[off].item())
+    view[off] = old ^ mask
+    try:
+        assert not pipe.run(root), "a flipped weight byte went undetected"
+        mism = hv.hv_compare_roots(pipe.roots, clean_roots).cpu().numpy()
+        assert list(np.nonzero(mism)[0]) == [m], "mismatch not localised to the flipped tensor"
+    finally:
+        view[off] = old
+    assert pipe.run(root)
+    bad = bytearray(root)
+    bad[int(rng.integers(0, 32))] ^= int(rng.integers(1, 256))
+    assert not pipe.run(bytes(bad))
