@@ -209,10 +209,15 @@ def main():
     }
     if not args.no_peaks:
         valu = hv.measure_valu_peak(dev)
+        sha = hv.measure_sha256_ceiling(dev)
         hbm = hv.measure_hbm_read(16 << 30, dev)
-        log(f"measured peaks: VALU mix {valu['tops']:.2f} TOP/s, HBM read {hbm['GBps']:.0f} GB/s")
+        kernel_blocks_per_s = blocks / (k_ms / 1e3)
+        log(f"measured peaks: VALU mix {valu['tops']:.2f} TOP/s, register-only SHA-256 "
+            f"{sha['GBps_equiv']:.0f} GB/s-equiv, HBM read {hbm['GBps']:.0f} GB/s")
         line["roofline"]["measured_valu_peak"] = round(valu["tops"], 3)
         line["roofline"]["frac_of_measured_valu_peak"] = round(achieved / valu["tops"], 4)
+        line["roofline"]["register_sha256_GBps"] = round(sha["GBps_equiv"], 1)
+        line["roofline"]["frac_of_register_sha256"] = round(kernel_blocks_per_s / sha["blocks_per_s"], 4)
         line["roofline"]["measured_hbm_read_GBps"] = round(hbm["GBps"], 1)
     if not args.no_cpu_baseline:
         log("cpu baseline ...")

@@ -25,6 +25,16 @@ extern "C" {
  * Errors: HV_ERR_INVALID_ARG for NULL pointers or grid == 0; HV_ERR_HIP. */
 hv_status hv_mb_valu(uint32_t* sink, uint32_t grid, uint32_t iters, uint64_t* ops_per_launch, hipStream_t stream);
 
+/* SHA-256 compressions chained on registers only (FIPS 180-4 section 6.2.2
+ * rounds, no loads or stores in the loop): `blocks` per lane, `grid` blocks
+ * of 256 lanes.  The rate of this kernel is the ceiling of the leaf kernel's
+ * arithmetic on this chip at the clock it holds.
+ *   sink: device, grid * 256 uint32 (written).
+ *   blocks_per_launch: host, receives grid * 256 * blocks.
+ * Errors: HV_ERR_INVALID_ARG for NULL pointers or grid == 0; HV_ERR_HIP. */
+hv_status hv_mb_sha256(uint32_t* sink, uint32_t grid, uint32_t blocks, uint64_t* blocks_per_launch,
+                       hipStream_t stream);
+
 /* Streaming read of `nbytes` (a multiple of 16) at `buf` with 16-byte loads,
  * grid-stride, folded to one word per lane.
  *   buf: device, 16-byte aligned.   sink: device, grid * 256 uint32.

@@ -4,6 +4,7 @@
 
 #include "hv.h"
 #include "hv_microbench.h"
+#include "sha256_device.h"
 
 namespace {
 
@@ -50,6 +51,28 @@ __global__ void __launch_bounds__(kThreads) hbm_read_kernel(const uint4* __restr
     sink[tid] = acc;
 }
 
+// SHA-256 compressions on registers only: each lane chains `blocks`
+// compressions of a block derived from its own state, with no memory traffic
+// in the loop -- the ceiling the leaf kernel's arithmetic can reach.
+__global__ void __launch_bounds__(kThreads) sha256_registers_kernel(uint32_t* __restrict__ sink, uint32_t blocks) {
+    const uint32_t tid = blockIdx.x * kThreads + threadIdx.x;
+    uint32_t H[8];
+    hv::init_state(H);
+    uint32_t M[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) M[i] = tid * 16u + (uint32_t)i;
+    for (uint32_t b = 0; b < blocks; ++b) {
+        uint32_t W[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) W[i] = M[i] ^ H[i & 7];
+        hv::compress(H, W);
+    }
+    uint32_t r = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r ^= H[i];
+    sink[tid] = r;
+}
+
 }  // namespace
 
 extern "C" {
@@ -58,6 +81,14 @@ hv_status hv_mb_valu(uint32_t* sink, uint32_t grid, uint32_t iters, uint64_t* op
     if (sink == nullptr || ops_per_launch == nullptr || grid == 0) return HV_ERR_INVALID_ARG;
     valu_mix_kernel<<<grid, kThreads, 0, stream>>>(sink, iters, 0x2510u);
     *ops_per_launch = (uint64_t)grid * kThreads * iters * kChains * kOpsPerChain;
+    return hipGetLastError() == hipSuccess ? HV_OK : HV_ERR_HIP;
+}
+
+hv_status hv_mb_sha256(uint32_t* sink, uint32_t grid, uint32_t blocks, uint64_t* blocks_per_launch,
+                       hipStream_t stream) {
+    if (sink == nullptr || blocks_per_launch == nullptr || grid == 0) return HV_ERR_INVALID_ARG;
+    sha256_registers_kernel<<<grid, kThreads, 0, stream>>>(sink, blocks);
+    *blocks_per_launch = (uint64_t)grid * kThreads * blocks;
     return hipGetLastError() == hipSuccess ? HV_OK : HV_ERR_HIP;
 }
 

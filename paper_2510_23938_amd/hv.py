@@ -40,7 +40,7 @@ EXPORTS = (
     "hv_merkle_reduce", "hv_verify_workspace_bytes", "hv_verify_root", "hv_compare_roots",
     "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
     "hv_leaf_schedule",  # include/hv_inspect.h
-    "hv_mb_valu", "hv_mb_hbm_read",  # include/hv_microbench.h
+    "hv_mb_valu", "hv_mb_sha256", "hv_mb_hbm_read",  # include/hv_microbench.h
 )
 
 
@@ -80,6 +80,7 @@ def _load():
         "hv_leaf_schedule": ([vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
         "hv_mb_valu": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_hbm_read": ([vp, u64, vp, u32, vp], ctypes.c_int),
+        "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -229,6 +230,26 @@ def measure_valu_peak(device="cuda", grid=16384, iters=4096, reps=5) -> dict:
         ms = a.elapsed_time(b)
         best = ms if best is None else min(best, ms)
     return {"tops": ops.value / (best / 1e3) / 1e12, "ms": best, "ops": ops.value, "grid": grid, "iters": iters}
+
+
+def measure_sha256_ceiling(device="cuda", grid=8192, blocks=256, reps=5) -> dict:
+    """Best rate of register-only SHA-256 compressions (no memory traffic)."""
+    dev = torch.device(device)
+    sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
+    n = ctypes.c_uint64(0)
+    s = _stream(dev)
+    _check(lib.hv_mb_sha256(sink.data_ptr(), grid, 8, ctypes.byref(n), s))  # warm-up
+    best = None
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        _check(lib.hv_mb_sha256(sink.data_ptr(), grid, blocks, ctypes.byref(n), s))
+        b.record()
+        b.synchronize()
+        ms = a.elapsed_time(b)
+        best = ms if best is None else min(best, ms)
+    return {"blocks_per_s": n.value / (best / 1e3), "GBps_equiv": n.value * 64 / (best / 1e3) / 1e9, "ms": best,
+            "blocks": n.value}
 
 
 def measure_hbm_read(nbytes=16 << 30, device="cuda", grid=None, reps=5) -> dict:

@@ -23,7 +23,7 @@ def declared_functions():
 
     text = "".join(open(f).read() for f in sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))))
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(hv_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(hv_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_every_declared_symbol_is_exported():
