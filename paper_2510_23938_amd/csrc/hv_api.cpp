@@ -11,9 +11,10 @@
 
 #include <vector>
 
+#include "hv_host.h"
 #include "hv_kernels.h"
 
-namespace {
+namespace hvh {
 
 thread_local char g_error[512] = "";
 
@@ -28,38 +29,6 @@ hv_status fail(hv_status st, const char* fmt, ...) {
 hv_status hip_fail(hipError_t e, const char* what) {
     return fail(HV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
-
-constexpr size_t kAlign = 256;
-size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-
-// Largest leaf count one call accepts: the hash grid is 256 lanes per block
-// in a 32-bit block index.
-constexpr uint64_t kMaxLeaves = (uint64_t)1 << 38;
-// Largest chunk: the leaf kernel counts a chunk's 64-byte blocks in 32 bits.
-constexpr uint64_t kMaxChunkBytes = ((uint64_t)1 << 38) - 64;
-
-// Carves consecutive 256-byte-aligned regions out of a workspace.
-struct Carver {
-    uint8_t* base;
-    size_t used = 0;
-    explicit Carver(void* b) : base(static_cast<uint8_t*>(b)) {}
-    template <typename T>
-    T* take(size_t count) {
-        T* p = reinterpret_cast<T*>(base ? base + used : nullptr);
-        used += round_up(count * sizeof(T));
-        return p;
-    }
-};
-
-struct HashLayout {
-    hv::MsgDesc* msgs;
-    hv::Pair* cnt;
-    hv::Pair* off;
-    hv::Pair* partials;
-    uint64_t* hist;
-    hv::LeafDesc* desc;
-    size_t bytes;
-};
 
 HashLayout hash_layout(void* ws, uint32_t n_msgs, uint64_t n_leaves) {
     Carver c(ws);
@@ -108,6 +77,12 @@ hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_
     return HV_OK;
 }
 
+}  // namespace hvh
+
+using namespace hvh;
+
+namespace {
+
 struct Timing {
     bool enabled = false;
     bool have = false;
@@ -142,6 +117,33 @@ MerkleLayout merkle_layout(void* ws, uint64_t n_nodes, uint32_t n_seg) {
     return L;
 }
 
+}  // namespace
+
+namespace hvh {
+
+// Scheduling kernels over device-resident descriptors: the leaf table of
+// n_msgs messages goes to L.desc (which must be sized for n_leaves).
+hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t n_full,
+                         uint64_t n_leaves, const HashLayout& L, hipStream_t stream) {
+    hipError_t e;
+    if ((e = hv::launch_sched_count(msgs_dev, n_msgs, chunk_bytes, L.cnt, stream)) != hipSuccess)
+        return hip_fail(e, "count kernel");
+    if ((e = hv::launch_scan_pairs(L.cnt, L.off, n_msgs, L.partials, stream)) != hipSuccess)
+        return hip_fail(e, "scan kernels");
+    if (n_full > 0 &&
+        (e = hv::launch_sched_full(msgs_dev, L.off, n_msgs, chunk_bytes, n_full, L.desc, stream)) != hipSuccess)
+        return hip_fail(e, "full-chunk kernel");
+    if (n_leaves > n_full &&
+        (e = hv::launch_sched_tails(msgs_dev, L.off, n_msgs, chunk_bytes, n_full, L.hist, L.desc, stream)) !=
+            hipSuccess)
+        return hip_fail(e, "tail sort kernels");
+    return HV_OK;
+}
+
+}  // namespace hvh
+
+namespace {
+
 // Validation plus the scheduling kernels shared by hv_hash_chunks and
 // hv_leaf_schedule.  On HV_OK the leaf table is queued into L.desc.
 hv_status schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, bool need_out, const void* out,
@@ -168,18 +170,7 @@ hv_status schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, bo
     static_assert(sizeof(hv_msg) == sizeof(hv::MsgDesc), "hv_msg layout");
     hipError_t e = hipMemcpyAsync(L.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "descriptor upload");
-    if ((e = hv::launch_sched_count(L.msgs, n_msgs, chunk_bytes, L.cnt, stream)) != hipSuccess)
-        return hip_fail(e, "count kernel");
-    if ((e = hv::launch_scan_pairs(L.cnt, L.off, n_msgs, L.partials, stream)) != hipSuccess)
-        return hip_fail(e, "scan kernels");
-    if (n_full > 0 &&
-        (e = hv::launch_sched_full(L.msgs, L.off, n_msgs, chunk_bytes, n_full, L.desc, stream)) != hipSuccess)
-        return hip_fail(e, "full-chunk kernel");
-    if (n_leaves > n_full &&
-        (e = hv::launch_sched_tails(L.msgs, L.off, n_msgs, chunk_bytes, n_full, L.hist, L.desc, stream)) !=
-            hipSuccess)
-        return hip_fail(e, "tail sort kernels");
-    return HV_OK;
+    return hvh::queue_schedule(L.msgs, n_msgs, chunk_bytes, n_full, n_leaves, L, stream);
 }
 
 }  // namespace

@@ -1,0 +1,58 @@
+// hv_host.h -- host-side internals shared by the C-ABI sources: argument
+// errors, workspace carving and the scheduling launch sequence.
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+#include "hv.h"
+#include "hv_kernels.h"
+
+namespace hvh {
+
+constexpr size_t kAlign = 256;
+inline size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Largest leaf count one call accepts: the hash grid is 256 lanes per block
+// in a 32-bit block index.
+constexpr uint64_t kMaxLeaves = (uint64_t)1 << 38;
+// Largest chunk: the leaf kernel counts a chunk's 64-byte blocks in 32 bits.
+constexpr uint64_t kMaxChunkBytes = ((uint64_t)1 << 38) - 64;
+
+// Carves consecutive 256-byte-aligned regions out of a workspace.
+struct Carver {
+    uint8_t* base;
+    size_t used = 0;
+    explicit Carver(void* b) : base(static_cast<uint8_t*>(b)) {}
+    template <typename T>
+    T* take(size_t count) {
+        T* p = reinterpret_cast<T*>(base ? base + used : nullptr);
+        used += round_up(count * sizeof(T));
+        return p;
+    }
+};
+
+struct HashLayout {
+    hv::MsgDesc* msgs;
+    hv::Pair* cnt;
+    hv::Pair* off;
+    hv::Pair* partials;
+    uint64_t* hist;
+    hv::LeafDesc* desc;
+    size_t bytes;
+};
+
+HashLayout hash_layout(void* ws, uint32_t n_msgs, uint64_t n_leaves);
+
+// Records a detail string for hv_last_error() and returns st.
+hv_status fail(hv_status st, const char* fmt, ...);
+hv_status hip_fail(hipError_t e, const char* what);
+
+// Leaf counts of a message list (validation included); fills seg_offsets when given.
+hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_offsets, uint64_t* n_leaves,
+                 uint64_t* n_full);
+
+// Scheduling kernels over device-resident descriptors into L (leaf table in L.desc).
+hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t n_full,
+                         uint64_t n_leaves, const HashLayout& L, hipStream_t stream);
+
+}  // namespace hvh

@@ -41,6 +41,7 @@ EXPORTS = (
     "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
     "hv_leaf_schedule",  # include/hv_inspect.h
     "hv_mb_valu", "hv_mb_sha256", "hv_mb_hbm_read",  # include/hv_microbench.h
+    "hv_stream_workspace_bytes", "hv_hash_host_chunks",  # include/hv_stream.h
 )
 
 
@@ -81,6 +82,8 @@ def _load():
         "hv_mb_valu": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_hbm_read": ([vp, u64, vp, u32, vp], ctypes.c_int),
         "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
+        "hv_stream_workspace_bytes": ([vp, u32, u64, u64], sz),
+        "hv_hash_host_chunks": ([vp, u32, u64, vp, u64, vp, sz, vp, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -164,6 +167,43 @@ def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace |
     ws = (workspace or Workspace(dev)).get(lib.hv_hash_workspace_bytes(n, n_leaves))
     _check(lib.hv_hash_chunks(arr.ctypes.data if n else None, n, chunk_bytes, out.data_ptr() if n_leaves else None,
                               ws.data_ptr(), ws.numel(), _stream(dev)))
+    return out, seg
+
+
+def host_messages_of(arrays) -> tuple:
+    """(ptrs, lens) of host byte buffers: numpy arrays or CPU tensors (pinned ones let copies overlap hashing)."""
+    ptrs, lens = [], []
+    for a in arrays:
+        if isinstance(a, torch.Tensor):
+            if a.is_cuda or not a.is_contiguous():
+                raise ValueError("host messages must be contiguous CPU tensors")
+            ptrs.append(a.data_ptr())
+            lens.append(a.numel() * a.element_size())
+        else:
+            a = np.ascontiguousarray(a)
+            ptrs.append(a.ctypes.data if a.nbytes else 0)
+            lens.append(a.nbytes)
+    return np.array(ptrs, dtype=np.uint64), np.array(lens, dtype=np.uint64)
+
+
+def hv_hash_host_chunks(host_msgs, chunk_bytes: int, batch_bytes: int = 1 << 30, device="cuda",
+                        workspace: Workspace | None = None, copy_stream=None):
+    """Leaf digests of host-resident messages streamed through GPU memory
+    (synchronous): ([n_leaves, 32] uint8 device tensor, seg_offsets)."""
+    ptrs, lens = host_messages_of(host_msgs) if not (isinstance(host_msgs, tuple) and len(host_msgs) == 2
+                                                     and isinstance(host_msgs[0], np.ndarray)) else host_msgs
+    seg, n_leaves = hv_leaf_layout(ptrs, lens, chunk_bytes)
+    arr = _msg_array(ptrs, lens)
+    n = len(arr)
+    dev = torch.device(device)
+    need = lib.hv_stream_workspace_bytes(arr.ctypes.data if n else None, n, chunk_bytes, batch_bytes)
+    if need == 0:
+        raise HVError(HV_ERR_INVALID_ARG, lib.hv_last_error().decode("utf-8", "replace"))
+    ws = (workspace or Workspace(dev)).get(need)
+    out = torch.empty((n_leaves, 32), dtype=torch.uint8, device=dev)
+    cs = copy_stream or torch.cuda.Stream(dev)
+    _check(lib.hv_hash_host_chunks(arr.ctypes.data if n else None, n, chunk_bytes, out.data_ptr() if n_leaves else None,
+                                   batch_bytes, ws.data_ptr(), ws.numel(), cs.cuda_stream, _stream(dev)))
     return out, seg
 
 

@@ -148,6 +148,18 @@ def test_verify_rejects_before_launch():
     assert hv.lib.hv_compare_roots(None, None, 3, None, None) == hv.HV_ERR_INVALID_ARG
 
 
+def test_stream_plan_sizes_and_rejections():
+    ptrs, lens = _msgs([1 << 20, 100, 0])
+    arr = hv._msg_array(ptrs, lens)
+    ok = hv.lib.hv_stream_workspace_bytes(arr.ctypes.data, 3, 65536, 1 << 20)
+    assert ok >= 2 << 20 and ok % 256 == 0
+    assert hv.lib.hv_stream_workspace_bytes(arr.ctypes.data, 3, 65536, 1000) == 0      # not a multiple of 256
+    assert b"multiple of 256" in hv.lib.hv_last_error()
+    assert hv.lib.hv_stream_workspace_bytes(arr.ctypes.data, 3, 0, 1 << 19) == 0       # whole message > batch
+    assert b"does not fit" in hv.lib.hv_last_error()
+    assert hv.lib.hv_stream_workspace_bytes(arr.ctypes.data, 3, 100, 1 << 20) == 0     # bad chunk size
+
+
 def test_timing_query_without_timed_call():
     with pytest.raises(hv.HVError):
         hv.leaf_kernel_ms()
