@@ -191,6 +191,62 @@ def stream_bench(args, dev):
     }), flush=True)
 
 
+def incremental_bench(args, dev):
+    """Re-verification after K chunks change: rehash K chunks, update their branches, manifest, verify."""
+    import torch
+    import workloads as W
+    from paper_2510_23938_amd import hv
+
+    wl = W.workload(args.config, dev)
+    C = wl.chunk_bytes
+    msgs = wl.msgs
+    leaves, seg = hv.hv_hash_chunks(msgs, C, dev)
+    tree = hv.Tree(leaves, seg)
+    n_seg = len(seg) - 1
+    top_seg = np.array([0, n_seg], dtype=np.uint64)
+    rng = np.random.default_rng(W.seed_of(args.config) + 7)
+    n_leaves = int(seg[-1])
+    k = min(args.incremental, n_leaves)
+    pipe = hv.Pipeline(msgs, C, "manifest", dev)  # full re-verification, for time and for the expected root
+    rehash_ws, top_ws = hv.Workspace(dev), hv.Workspace(dev)
+    inc_ms, full_ms = [], []
+    for rep in range(args.warmup + args.steps):
+        dirty = np.sort(rng.choice(n_leaves, size=k, replace=False)).astype(np.uint64)
+        owners = np.searchsorted(seg, dirty, side="right") - 1
+        for leaf, m in zip(dirty, owners):     # flip one byte inside each chosen chunk
+            off = (int(leaf) - int(seg[m])) * C if C else 0
+            v = msgs.views[m] if msgs.views is not None else None
+            if v is not None:
+                v[off] ^= 0x01
+            else:
+                o = int(msgs.offsets[m]) + off
+                msgs.buffer[o] ^= 0x01
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        hv.hv_rehash_chunks(msgs, C, dirty, leaves, rehash_ws)
+        roots = tree.update(leaves, dirty)
+        top = hv.hv_merkle_reduce(roots, top_seg, top_ws)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        expected = bytes(pipe.compute().cpu().numpy().reshape(-1))
+        t2 = time.perf_counter()
+        assert hv.hv_verify_root(top, expected), "incremental root differs from the full recompute"
+        if rep >= args.warmup:
+            inc_ms.append((t1 - t0) * 1e3)
+            full_ms.append((t2 - t1) * 1e3)
+    inc, full = float(np.median(inc_ms)), float(np.median(full_ms))
+    log(f"incremental: {k} changed chunks of {n_leaves}: {inc:.3f} ms vs full {full:.2f} ms ({full / inc:.1f}x)")
+    print(json.dumps({
+        "metric": "ms to re-verify after K changed chunks (rehash K + branch update + manifest), 1 MI355X",
+        "value": round(inc, 4), "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(inc, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u32", "data": "synthetic",
+        "config": {"workload": wl.description, "changed_chunks": k, "leaves": n_leaves, "chunk_bytes": C,
+                   "full_reverify_ms": round(full, 3), "speedup": round(full / inc, 2),
+                   "matches_full_recompute": True},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -204,6 +260,9 @@ def main():
                     help="instead: stream this many GiB of the 70B-shaped tensors from pinned host memory "
                          "(host-to-device copy + hash + roots + verify per step)")
     ap.add_argument("--batch-mib", type=int, default=1024, help="staging batch for --stream")
+    ap.add_argument("--incremental", type=int, default=0, metavar="K",
+                    help="instead: change K random chunks of the workload and time re-verification that rehashes "
+                         "only them and updates only their tree branches, against a full re-verification")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 4 GiB device copy first (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -221,6 +280,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.stream > 0:
         stream_bench(args, dev)
+        return
+    if args.incremental > 0:
+        incremental_bench(args, dev)
         return
     if args.copy_calibration:
         a = torch.empty(4 << 30, dtype=torch.uint8, device=dev)

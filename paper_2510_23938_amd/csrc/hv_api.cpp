@@ -204,7 +204,7 @@ hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_byt
         if (!T.stop && (e = hipEventCreate(&T.stop)) != hipSuccess) return hip_fail(e, "event create");
         if ((e = hipEventRecord(T.start, stream)) != hipSuccess) return hip_fail(e, "event record");
     }
-    if ((e = hv::launch_sha256_leaves(L.desc, n_leaves, leaf_digests, stream)) != hipSuccess)
+    if ((e = hv::launch_sha256_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream)) != hipSuccess)
         return hip_fail(e, "sha256 leaf kernel");
     if (T.enabled) {
         if ((e = hipEventRecord(T.stop, stream)) != hipSuccess) return hip_fail(e, "event record");

@@ -36,8 +36,16 @@ hipError_t launch_sched_full(const MsgDesc* msgs, const Pair* off, uint32_t n, u
 hipError_t launch_sched_tails(const MsgDesc* msgs, const Pair* off, uint32_t n, uint64_t C, uint64_t n_full,
                               uint64_t* hist, LeafDesc* desc, hipStream_t s);
 
-// SHA-256 of every leaf (sha256_leaves.hip).
-hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_leaves, uint8_t* digests, hipStream_t s);
+// Leaf table for a sorted list of leaf numbers (sched.hip): desc[e] is leaf
+// leaves[e], located through the per-message offsets `off` (first leaf of
+// message m = off[m].x + off[m].y).
+hipError_t launch_sched_select(const MsgDesc* msgs, const Pair* off, uint32_t n, uint64_t C, const uint64_t* leaves,
+                               uint64_t k, LeafDesc* desc, hipStream_t s);
+
+// SHA-256 of the n_slots leaves of a leaf table (sha256_leaves.hip); digests
+// go to digests + 32 * desc.out for desc.out < out_bound.
+hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
+                                hipStream_t s);
 
 // Merkle tiles (merkle.hip).  One launch reduces every segment by up to
 // kTileLevels levels: tile t covers up to 2^kTileLevels consecutive nodes of
@@ -46,6 +54,20 @@ constexpr int kTileLevels = 9;
 constexpr int kTileNodes = 1 << kTileLevels;
 hipError_t launch_merkle_tiles(const uint8_t* in, uint8_t* out, const uint64_t* in_off, const uint64_t* tile_off,
                                uint32_t n_seg, uint64_t n_tiles, int leaf_mode, hipStream_t s);
+
+// Persistent tree for incremental updates (tree.hip).
+hipError_t launch_tree_leaf_level(const uint8_t* digests, uint64_t n, uint8_t* level0, hipStream_t s);
+hipError_t launch_tree_build_level(const uint8_t* in, uint8_t* out, const uint64_t* in_off, const uint64_t* out_off,
+                                   uint32_t n_seg, uint64_t n_out, hipStream_t s);
+hipError_t launch_tree_locate(const uint64_t* dirty, uint32_t k, const uint64_t* seg_off, uint32_t n_seg,
+                              uint32_t* seg_of, uint64_t* local, hipStream_t s);
+hipError_t launch_tree_update_leaves(const uint8_t* digests, const uint64_t* dirty, uint32_t k, uint8_t* level0,
+                                     hipStream_t s);
+hipError_t launch_tree_update_level(const uint8_t* in, uint8_t* out, const uint64_t* in_off, const uint64_t* out_off,
+                                    const uint32_t* seg_of, const uint64_t* local, uint32_t k, uint32_t shift,
+                                    hipStream_t s);
+hipError_t launch_tree_roots(const uint8_t* top, const uint64_t* top_off, uint32_t n_seg, uint8_t* roots,
+                             hipStream_t s);
 
 // Verification (verify.hip).
 hipError_t launch_verify_root(const uint8_t* root, const uint32_t expected_le[8], uint32_t* flag, hipStream_t s);

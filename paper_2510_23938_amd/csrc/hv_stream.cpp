@@ -193,7 +193,7 @@ hv_status hv_hash_host_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chun
         st = queue_schedule(L.descs + B.p0, (uint32_t)(B.p1 - B.p0), chunk_bytes, B.n_full, B.n_leaves, L.hash,
                             hash_stream);
         if (st != HV_OK) break;
-        if ((e = hv::launch_sha256_leaves(L.hash.desc, B.n_leaves, leaf_digests + 32 * B.first_leaf, hash_stream)) !=
+        if ((e = hv::launch_sha256_leaves(L.hash.desc, B.n_leaves, B.n_leaves, leaf_digests + 32 * B.first_leaf, hash_stream)) !=
                 hipSuccess ||
             (e = hipEventRecord(hashed[buf], hash_stream)) != hipSuccess)
             st = hip_fail(e, "sha256 leaf kernel");

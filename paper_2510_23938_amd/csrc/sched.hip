@@ -191,6 +191,39 @@ __global__ void __launch_bounds__(kThreads) tail_scatter_kernel(const MsgDesc* _
     }
 }
 
+// The message holding leaf number `leaf`: the last m with first(m) <= leaf,
+// first(m) = off[m].x + off[m].y (messages without leaves share their
+// successor's first leaf and are skipped by taking the last).
+__device__ __forceinline__ uint32_t find_leaf_owner(const Pair* __restrict__ off, uint32_t n, uint64_t leaf) {
+    uint32_t lo = 0, hi = n;
+    while (hi - lo > 1) {
+        const uint32_t mid = lo + (hi - lo) / 2;
+        if (off[mid].x + off[mid].y <= leaf) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+__global__ void __launch_bounds__(kThreads) select_kernel(const MsgDesc* __restrict__ msgs, const Pair* __restrict__ off,
+                                                          uint32_t n, uint64_t C, const uint64_t* __restrict__ leaves,
+                                                          uint64_t k, LeafDesc* __restrict__ desc) {
+    for (uint64_t e = (uint64_t)blockIdx.x * kThreads + threadIdx.x; e < k; e += (uint64_t)gridDim.x * kThreads) {
+        const uint64_t leaf = leaves[e];
+        const uint32_t m = find_leaf_owner(off, n, leaf);
+        const MsgDesc msg = msgs[m];
+        const uint64_t i = leaf - (off[m].x + off[m].y);
+        LeafDesc d;
+        if (C == 0) {
+            d.src = msg.data;
+            d.nbytes = msg.nbytes;
+        } else {
+            d.src = msg.data + i * C;
+            d.nbytes = msg.nbytes - i * C < C ? msg.nbytes - i * C : C;
+        }
+        d.out = leaf;
+        desc[e] = d;
+    }
+}
+
 unsigned grid_for(uint64_t n) {
     const uint64_t blocks = (n + kThreads - 1) / kThreads;
     const uint64_t cap = 65536;  // grid-stride loops cover the rest
@@ -226,6 +259,13 @@ hipError_t launch_scan_pairs(const Pair* in, Pair* out, size_t n, Pair* partials
 hipError_t launch_sched_full(const MsgDesc* msgs, const Pair* off, uint32_t n, uint64_t C, uint64_t n_full,
                              LeafDesc* desc, hipStream_t s) {
     full_kernel<<<grid_for(n_full), kThreads, 0, s>>>(msgs, off, n, C, n_full, desc);
+    return hipGetLastError();
+}
+
+hipError_t launch_sched_select(const MsgDesc* msgs, const Pair* off, uint32_t n, uint64_t C, const uint64_t* leaves,
+                               uint64_t k, LeafDesc* desc, hipStream_t s) {
+    if (k == 0) return hipSuccess;
+    select_kernel<<<grid_for(k), kThreads, 0, s>>>(msgs, off, n, C, leaves, k, desc);
     return hipGetLastError();
 }
 

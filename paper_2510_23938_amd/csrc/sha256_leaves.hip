@@ -172,11 +172,11 @@ __device__ __forceinline__ void final_blocks(uint32_t H[8], const uint8_t* p, ui
     }
 }
 
-__global__ void __launch_bounds__(kThreads) sha256_leaves_kernel(const LeafDesc* __restrict__ desc, uint64_t n_leaves,
-                                                                 uint8_t* __restrict__ digests) {
+__global__ void __launch_bounds__(kThreads) sha256_leaves_kernel(const LeafDesc* __restrict__ desc, uint64_t n_slots,
+                                                                 uint64_t out_bound, uint8_t* __restrict__ digests) {
     __shared__ __attribute__((aligned(16))) uint8_t stage[kWaves][64 * kStageBytes];
     const uint64_t slot = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-    const bool live = slot < n_leaves;
+    const bool live = slot < n_slots;
     LeafDesc d = {0, 0, 0};
     if (live) d = desc[slot];
     const uint8_t* p = reinterpret_cast<const uint8_t*>(d.src);
@@ -191,15 +191,16 @@ __global__ void __launch_bounds__(kThreads) sha256_leaves_kernel(const LeafDesc*
         full_blocks_any(H, p, nfull);
     }
     final_blocks(H, p + ((uint64_t)nfull << 6), (uint32_t)(d.nbytes & 63), d.nbytes);
-    if (live && d.out < n_leaves) store_digest(digests + 32 * d.out, H);
+    if (live && d.out < out_bound) store_digest(digests + 32 * d.out, H);
 }
 
 }  // namespace
 
-hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_leaves, uint8_t* digests, hipStream_t s) {
-    if (n_leaves == 0) return hipSuccess;
-    const uint64_t blocks = (n_leaves + kThreads - 1) / kThreads;
-    sha256_leaves_kernel<<<(unsigned)blocks, kThreads, 0, s>>>(desc, n_leaves, digests);
+hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
+                                hipStream_t s) {
+    if (n_slots == 0) return hipSuccess;
+    const uint64_t blocks = (n_slots + kThreads - 1) / kThreads;
+    sha256_leaves_kernel<<<(unsigned)blocks, kThreads, 0, s>>>(desc, n_slots, out_bound, digests);
     return hipGetLastError();
 }
 

@@ -42,6 +42,8 @@ EXPORTS = (
     "hv_leaf_schedule",  # include/hv_inspect.h
     "hv_mb_valu", "hv_mb_sha256", "hv_mb_hbm_read",  # include/hv_microbench.h
     "hv_stream_workspace_bytes", "hv_hash_host_chunks",  # include/hv_stream.h
+    "hv_tree_bytes", "hv_tree_build", "hv_tree_update_workspace_bytes", "hv_tree_update",
+    "hv_rehash_workspace_bytes", "hv_rehash_chunks",  # include/hv_incremental.h
 )
 
 
@@ -84,6 +86,12 @@ def _load():
         "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_stream_workspace_bytes": ([vp, u32, u64, u64], sz),
         "hv_hash_host_chunks": ([vp, u32, u64, vp, u64, vp, sz, vp, vp], ctypes.c_int),
+        "hv_tree_bytes": ([vp, u32], sz),
+        "hv_tree_build": ([vp, vp, u32, vp, sz, vp, vp], ctypes.c_int),
+        "hv_tree_update_workspace_bytes": ([u32], sz),
+        "hv_tree_update": ([vp, vp, u32, vp, sz, vp, u32, vp, vp, sz, vp], ctypes.c_int),
+        "hv_rehash_workspace_bytes": ([u32, u32], sz),
+        "hv_rehash_chunks": ([vp, u32, u64, vp, u32, vp, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -410,6 +418,58 @@ class Pipeline:
         """The whole path: digests, roots, comparison with ``expected`` (synchronous)."""
         root = self.compute()
         return hv_verify_root(root, expected, _FixedWorkspace(self.ws_verify))
+
+
+class Tree:
+    """A persistent per-segment Merkle tree on the device (include/hv_incremental.h)."""
+
+    def __init__(self, leaf_digests: torch.Tensor, seg_offsets, roots: torch.Tensor | None = None):
+        self.seg = np.ascontiguousarray(seg_offsets, dtype=np.uint64)
+        self.n_seg = len(self.seg) - 1
+        self.device = leaf_digests.device
+        nbytes = lib.hv_tree_bytes(self.seg.ctypes.data, self.n_seg)
+        if nbytes == 0:
+            raise HVError(HV_ERR_INVALID_ARG, lib.hv_last_error().decode("utf-8", "replace"))
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self.roots = roots if roots is not None else torch.empty((self.n_seg, 32), dtype=torch.uint8,
+                                                                 device=self.device)
+        self.ws = Workspace(self.device)
+        _check(lib.hv_tree_build(leaf_digests.data_ptr() if leaf_digests.numel() else None, self.seg.ctypes.data,
+                                 self.n_seg, self.buf.data_ptr(), self.buf.numel(), self.roots.data_ptr(),
+                                 _stream(self.device)))
+
+    def update(self, leaf_digests: torch.Tensor, dirty) -> torch.Tensor:
+        """Recompute the branches above the listed leaves (sorted unique leaf numbers); returns roots."""
+        d = np.ascontiguousarray(dirty, dtype=np.uint64)
+        ws = self.ws.get(lib.hv_tree_update_workspace_bytes(len(d)))
+        _check(lib.hv_tree_update(leaf_digests.data_ptr() if leaf_digests.numel() else None, self.seg.ctypes.data,
+                                  self.n_seg, self.buf.data_ptr(), self.buf.numel(),
+                                  d.ctypes.data if len(d) else None, len(d), self.roots.data_ptr(),
+                                  ws.data_ptr(), ws.numel(), _stream(self.device)))
+        return self.roots
+
+
+def hv_rehash_chunks(msgs, chunk_bytes: int, leaves, leaf_digests: torch.Tensor, workspace: Workspace | None = None):
+    """Recompute leaf_digests[j] for the listed leaf numbers j (sorted, unique) only."""
+    ptrs, lens = _ptr_len(msgs)
+    arr = _msg_array(ptrs, lens)
+    n = len(arr)
+    lst = np.ascontiguousarray(leaves, dtype=np.uint64)
+    ws = (workspace or Workspace(leaf_digests.device)).get(lib.hv_rehash_workspace_bytes(n, len(lst)))
+    _check(lib.hv_rehash_chunks(arr.ctypes.data if n else None, n, chunk_bytes, lst.ctypes.data if len(lst) else None,
+                                len(lst), leaf_digests.data_ptr() if leaf_digests.numel() else None,
+                                ws.data_ptr(), ws.numel(), _stream(leaf_digests.device)))
+    return leaf_digests
+
+
+def leaves_of_range(seg_offsets, chunk_bytes: int, msg: int, lo: int, hi: int) -> np.ndarray:
+    """Leaf numbers of the chunks of message `msg` that hold any byte in [lo, hi)."""
+    first = int(seg_offsets[msg])
+    if hi <= lo:
+        return np.zeros(0, dtype=np.uint64)
+    if chunk_bytes == 0:
+        return np.array([first], dtype=np.uint64)
+    return np.arange(first + lo // chunk_bytes, first + (hi - 1) // chunk_bytes + 1, dtype=np.uint64)
 
 
 class _FixedWorkspace:

@@ -160,6 +160,22 @@ def test_stream_plan_sizes_and_rejections():
     assert hv.lib.hv_stream_workspace_bytes(arr.ctypes.data, 3, 100, 1 << 20) == 0     # bad chunk size
 
 
+def test_incremental_rejects_before_launch():
+    seg = np.array([0, 10, 30], dtype=np.uint64)
+    assert hv.lib.hv_tree_bytes(seg.ctypes.data, 2) > 0
+    assert hv.lib.hv_tree_bytes(np.array([1, 2], dtype=np.uint64).ctypes.data, 1) == 0
+    for bad in ([3, 2], [5, 30], [4, 4]):
+        d = np.array(bad, dtype=np.uint64)
+        st = hv.lib.hv_tree_update(0x1000, seg.ctypes.data, 2, 0x100000, 1 << 20, d.ctypes.data, 2, 0x2000,
+                                   0x200000, 1 << 20, None)
+        assert st == hv.HV_ERR_INVALID_ARG
+    ptrs, lens = _msgs([1000, 64])
+    arr = hv._msg_array(ptrs, lens)
+    d = np.array([1, 0], dtype=np.uint64)
+    st = hv.lib.hv_rehash_chunks(arr.ctypes.data, 2, 64, d.ctypes.data, 2, 0x2000, 0x200000, 1 << 20, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"increasing" in hv.lib.hv_last_error()
+
+
 def test_timing_query_without_timed_call():
     with pytest.raises(hv.HVError):
         hv.leaf_kernel_ms()
