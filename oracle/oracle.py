@@ -60,6 +60,16 @@ def _load():
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int,
     ]
     lib.oracle_leaf_digests_mt.restype = ctypes.c_uint64
+    lib.oracle_leaf_digests_alg_mt.argtypes = [
+        ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int,
+    ]
+    lib.oracle_leaf_digests_alg_mt.restype = ctypes.c_uint64
+    lib.oracle_sha384.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p]
+    lib.oracle_sha384.restype = None
+    lib.oracle_mth384.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p]
+    lib.oracle_mth384.restype = None
+    lib.oracle_constants512.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    lib.oracle_constants512.restype = None
     _lib = lib
     return lib
 
@@ -87,6 +97,29 @@ def constants():
     return [int(x) for x in K], [int(x) for x in H]
 
 
+ALGS = {"sha256": (0, 32, 64), "sha384": (1, 48, 128)}  # id, digest bytes, block bytes
+
+
+def constants512():
+    """(K[0..79], H0[0..7]) of SHA-512 / SHA-384 exactly as the oracle holds them (FIPS 180-4 4.2.3, 5.3.4)."""
+    K = np.zeros(80, dtype=np.uint64)
+    H = np.zeros(8, dtype=np.uint64)
+    _load().oracle_constants512(K.ctypes.data, H.ctypes.data)
+    return [int(x) for x in K], [int(x) for x in H]
+
+
+def sha384(data) -> bytes:
+    """FIPS 180-4 SHA-384 of the bytes."""
+    a = _as_u8(data)
+    out = np.zeros(48, dtype=np.uint8)
+    _load().oracle_sha384(_ptr(a), a.size, out.ctypes.data)
+    return out.tobytes()
+
+
+def digest(data, alg: str = "sha256") -> bytes:
+    return sha256(data) if alg == "sha256" else sha384(data)
+
+
 def sha256(data) -> bytes:
     """FIPS 180-4 SHA-256 of the bytes."""
     a = _as_u8(data)
@@ -95,11 +128,12 @@ def sha256(data) -> bytes:
     return out.tobytes()
 
 
-def chunk_count(length: int, C: int) -> int:
-    """Algorithm 1's chunk_count = ceil(|M| / C); C = 0: one chunk (the whole message)."""
+def chunk_count(length: int, C: int, alg: str = "sha256") -> int:
+    """Algorithm 1's chunk_count = ceil(|M| / C); C = 0: one chunk (the whole message).
+    C must be a multiple of the hash's block (64 bytes for SHA-256, 128 for SHA-384)."""
     n = _load().oracle_chunk_count(length, C)
-    if n == UINT64_MAX:
-        raise ValueError(f"chunk size {C} is not a multiple of 64")
+    if n == UINT64_MAX or (C % ALGS[alg][2]):
+        raise ValueError(f"chunk size {C} is not a multiple of {ALGS[alg][2]}")
     return int(n)
 
 
@@ -113,15 +147,18 @@ def chunk_digests(data, C: int) -> np.ndarray:
     return out
 
 
-def mth(entries) -> bytes:
-    """RFC 6962 Merkle Tree Hash over 32-byte entries ([n, 32] uint8 or list of bytes)."""
+def mth(entries, alg: str = "sha256") -> bytes:
+    """RFC 6962 Merkle Tree Hash over 32-byte (SHA-256) or 48-byte (SHA-384)
+    entries ([n, D] uint8 or list of bytes)."""
+    D = ALGS[alg][1]
     if isinstance(entries, (list, tuple)):
         e = np.frombuffer(b"".join(entries), dtype=np.uint8) if entries else np.zeros(0, np.uint8)
     else:
         e = np.ascontiguousarray(entries, dtype=np.uint8).reshape(-1)
-    assert e.size % 32 == 0
-    out = np.zeros(32, dtype=np.uint8)
-    _load().oracle_mth(_ptr(e), e.size // 32, out.ctypes.data)
+    assert e.size % D == 0
+    out = np.zeros(D, dtype=np.uint8)
+    f = _load().oracle_mth if alg == "sha256" else _load().oracle_mth384
+    f(_ptr(e), e.size // D, out.ctypes.data)
     return out.tobytes()
 
 
@@ -144,12 +181,12 @@ def verify(root: bytes, expected: bytes) -> bool:
     return bytes(root) == bytes(expected)
 
 
-def leaf_digests_mt(messages, C: int, nthreads: int) -> np.ndarray:
-    """[n_leaves, 32]: chunk digests of all messages (message-major), on nthreads threads."""
+def leaf_digests_mt(messages, C: int, nthreads: int, alg: str = "sha256") -> np.ndarray:
+    """[n_leaves, D]: chunk digests of all messages (message-major), on nthreads threads."""
     arrs = [_as_u8(m) for m in messages]
     ptrs = np.array([a.ctypes.data if a.size else 0 for a in arrs], dtype=np.uint64)
     lens = np.array([a.size for a in arrs], dtype=np.uint64)
-    return _leaf_digests_raw(ptrs, lens, C, nthreads)
+    return _leaf_digests_raw(ptrs, lens, C, nthreads, alg)
 
 
 def leaf_digests_mt_packed(buf: np.ndarray, offsets, lens, C: int, nthreads: int) -> np.ndarray:
@@ -163,28 +200,39 @@ def leaf_digests_mt_packed(buf: np.ndarray, offsets, lens, C: int, nthreads: int
     return _leaf_digests_raw(ptrs, lens, C, nthreads)
 
 
-def _leaf_digests_raw(ptrs: np.ndarray, lens: np.ndarray, C: int, nthreads: int) -> np.ndarray:
+def _leaf_digests_raw(ptrs: np.ndarray, lens: np.ndarray, C: int, nthreads: int, alg: str = "sha256") -> np.ndarray:
     n = len(lens)
+    alg_id, D, _ = ALGS[alg]
     if C != 0:
-        chunk_count(0, C)  # validates C
+        chunk_count(0, C, alg)  # validates C
         total = int(np.sum(lens // np.uint64(C) + (lens % np.uint64(C) != 0))) if n else 0
     else:
         total = n
-    out = np.zeros((total, 32), dtype=np.uint8)
-    got = _load().oracle_leaf_digests_mt(ptrs.ctypes.data if n else None, lens.ctypes.data if n else None, n, C,
-                                         out.ctypes.data if total else None, nthreads)
+    out = np.zeros((total, D), dtype=np.uint8)
+    got = _load().oracle_leaf_digests_alg_mt(alg_id, ptrs.ctypes.data if n else None, lens.ctypes.data if n else None,
+                                             n, C, out.ctypes.data if total else None, nthreads)
     if got != total:
         raise RuntimeError("oracle_leaf_digests_mt failed")
     return out
 
 
-def seg_roots_from_leaves(leaves: np.ndarray, counts) -> list:
+def seg_roots_from_leaves(leaves: np.ndarray, counts, alg: str = "sha256") -> list:
     """Per-message roots from a message-major leaf array and per-message leaf counts."""
     roots, pos = [], 0
     for c in counts:
-        roots.append(mth(leaves[pos:pos + c]))
+        roots.append(mth(leaves[pos:pos + c], alg))
         pos += c
     return roots
+
+
+def chunk_digests_alg(data, C: int, alg: str = "sha256") -> np.ndarray:
+    """[n, D]: digest of each chunk in chunk order, for either hash."""
+    return leaf_digests_mt([data], C, 1, alg)
+
+
+def seg_root_alg(data, C: int, alg: str = "sha256") -> bytes:
+    """Root of one message for either hash: MTH over its chunk digests."""
+    return mth(chunk_digests_alg(data, C, alg), alg)
 
 
 def const_seg_root(length: int, C: int, byte: int) -> bytes:
