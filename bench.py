@@ -7,11 +7,12 @@ workload: the 70B-shaped bf16 weight set (723 tensors, 141.1 GB, 64 KiB
 chunks), generated on the GPU before timing; the bytes are already in HBM
 when the timed region starts.
 
-    python bench.py [--steps K] [--warmup W] [--config 1..5] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config 1..5] [--alg sha256|sha384] [--no-cpu-baseline]
 
-Also reported: the roofline of the dominant kernel (the SHA-256 leaf kernel,
-timed with HIP events on its own stream) against the integer-VALU peak, and
-the CPU oracle timed on a bounded sample of the same bytes on this host.
+Also reported: the roofline of the dominant kernel (the leaf kernel, timed
+with HIP events on its own stream) against the integer-VALU peak, and the CPU
+oracle timed on a bounded sample of the same bytes on this host.  With
+--alg sha384 every digest and node is SHA-384 (48 bytes, 128-byte blocks).
 """
 import argparse
 import hashlib
@@ -31,53 +32,66 @@ VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 # 32-bit VALU ops per SHA-256 block on gfx950 at the ISA minimum: 64 rounds x 14,
 # 48 schedule words x 10, 8 feed-forward adds, 16 byte swaps.
 OPS_PER_BLOCK = 64 * 14 + 48 * 10 + 8 + 16
-LEAF_KERNEL = "sha256_leaves_kernel"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sha256_leaves_traffic.json")
-KERNEL_SOURCES = ["paper_2510_23938_amd/csrc/sha256_leaves.hip", "paper_2510_23938_amd/csrc/sha256_device.h"]
+# The same for a SHA-384 block (128 bytes) with 64-bit words as 32-bit halves:
+# 80 rounds x (Sigma0, Sigma1: 6 alignbit + 2 bitop3 each; Ch, Maj: 2 bitop3
+# each; 7 64-bit adds as one v_lshl_add_u64 each), 64 schedule words x
+# (sigma0, sigma1: 8 each; 3 adds), 8 feed-forward adds, 32 byte swaps.
+OPS_PER_BLOCK_384 = 80 * 27 + 64 * 19 + 8 + 32
+CSRC = "paper_2510_23938_amd/csrc/"
+# per hash: block bytes, length-field bytes, ops per block, leaf kernel, traffic summary, kernel sources
+ALGS = {
+    "sha256": (64, 8, OPS_PER_BLOCK, "sha256_leaves_kernel", "sha256_leaves_traffic.json",
+               [CSRC + "sha256_leaves.hip", CSRC + "sha256_device.h"]),
+    "sha384": (128, 16, OPS_PER_BLOCK_384, "sha384_leaves_kernel", "sha384_leaves_traffic.json",
+               [CSRC + "sha384_leaves.hip", CSRC + "sha384_device.h"]),
+}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash():
+def kernel_source_hash(alg="sha256"):
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in ALGS[alg][5]:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def sha_blocks(lens, C):
-    """SHA-256 blocks the leaf kernel compresses (data + padding), from the chunk lengths."""
+def sha_blocks(lens, C, alg="sha256"):
+    """Blocks the leaf kernel compresses (data + padding: 0x80 and the length
+    field), from the message lengths and the chunk size."""
+    B, lf = ALGS[alg][0], ALGS[alg][1]
     lens = np.asarray(lens, dtype=np.uint64).astype(object)
     total = 0
     for L in lens:
         L = int(L)
         if C == 0:
-            total += (L + 72) // 64
+            total += (L + lf + B) // B
             continue
         full, tail = divmod(L, C)
-        total += full * ((C + 72) // 64)
+        total += full * ((C + lf + B) // B)
         if tail:
-            total += (tail + 72) // 64
+            total += (tail + lf + B) // B
     return total
 
 
-def traffic_for_current_kernel():
+def traffic_for_current_kernel(alg="sha256", config=5):
     """HBM bytes per leaf-kernel launch from the committed rocprofv3 counter
-    summary, or None when it is missing or was taken on different kernel code."""
+    summary, or None when it is missing, covers another workload or was taken
+    on different kernel code."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(os.path.join(ROOT, "profiles", ALGS[alg][4])) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_hash") != kernel_source_hash():
+    if rec.get("kernel_source_hash") != kernel_source_hash(alg) or rec.get("config", 5) != config:
         return None
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, pipe, sample_bytes):
+def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
     """The oracle (plain C, threaded over chunks) on the first whole chunks of
     the first messages, about sample_bytes in all; also checks those digests
     against the GPU's."""
@@ -102,9 +116,9 @@ def cpu_baseline(wl, pipe, sample_bytes):
     threads = min(16, len(os.sched_getaffinity(0)))
     nbytes = sum(h.size for h in host)
     t0 = time.perf_counter()
-    leaves = oracle.leaf_digests_mt(host, C, threads)
-    counts = [oracle.chunk_count(h.size, C) for h in host]
-    roots = oracle.seg_roots_from_leaves(leaves, counts)
+    leaves = oracle.leaf_digests_mt(host, C, threads, alg)
+    counts = [oracle.chunk_count(h.size, C, alg) for h in host]
+    roots = oracle.seg_roots_from_leaves(leaves, counts, alg)
     dt = time.perf_counter() - t0
     # the same leaves from the GPU run
     gpu = pipe.leaves.cpu().numpy()
@@ -253,6 +267,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=5)
+    ap.add_argument("--alg", choices=sorted(ALGS), default="sha256",
+                    help="hash of chunks and tree nodes (the resident path; --stream and --incremental use sha256)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-mib", type=int, default=3072)
     ap.add_argument("--no-peaks", action="store_true", help="skip the VALU / HBM peak microbenchmarks")
@@ -295,7 +311,9 @@ def main():
     torch.cuda.synchronize()
     log(f"workload {args.config}: {wl.description}; generated in {time.perf_counter() - t0:.1f} s")
     mode = "manifest" if wl.manifest else "single"
-    pipe = hv.Pipeline(wl.msgs, wl.chunk_bytes, mode, dev)
+    alg = args.alg
+    block_bytes, _, ops_per_block, leaf_kernel, _, _ = ALGS[alg]
+    pipe = hv.Pipeline(wl.msgs, wl.chunk_bytes, mode, dev, alg=alg)
 
     # warm-up; the first pass also fixes the expected root the timed passes verify against
     root = pipe.compute()
@@ -315,15 +333,15 @@ def main():
     hv.set_kernel_timing(False)
     # a flipped expected byte must fail, a matching one pass
     bad = bytearray(expected)
-    bad[int(np.random.default_rng(W.seed_of(args.config) + 1).integers(0, 32))] ^= 0x01
+    bad[int(np.random.default_rng(W.seed_of(args.config) + 1).integers(0, len(bad)))] ^= 0x01
     negative_ok = not pipe.run(bytes(bad))
 
     ms_step = dt / args.steps * 1e3
     total = pipe.total_bytes
     value = total / (ms_step / 1e3) / 1e9
     k_ms = float(np.mean(kernel_ms))
-    blocks = sha_blocks(wl.msgs.lens, wl.chunk_bytes)
-    achieved = blocks * OPS_PER_BLOCK / (k_ms / 1e3) / 1e12
+    blocks = sha_blocks(wl.msgs.lens, wl.chunk_bytes, alg)
+    achieved = blocks * ops_per_block / (k_ms / 1e3) / 1e12
     log(f"{args.steps} steps: {ms_step:.2f} ms/step, {value:.1f} GB/s; leaf kernel {k_ms:.2f} ms avg "
         f"({total / k_ms / 1e6:.1f} GB/s, {achieved:.2f} TOP/s)")
 
@@ -333,32 +351,33 @@ def main():
         "vs_baseline": None, "dtype": "u32", "data": "synthetic",
         "config": {
             "workload": wl.description, "config_index": args.config, "bytes": total, "messages": len(wl.msgs),
-            "leaves": pipe.n_leaves, "chunk_bytes": wl.chunk_bytes, "sha256_blocks": blocks,
+            "leaves": pipe.n_leaves, "chunk_bytes": wl.chunk_bytes, "hash": alg, f"{alg}_blocks": blocks,
             "verified": True, "mismatch_detected": negative_ok,
         },
         "roofline": {
-            "kernel": LEAF_KERNEL, "bound": "alu", "achieved": round(achieved, 3), "peak": round(VALU_PEAK_TOPS, 3),
-            "unit": "TOP/s", "frac": round(achieved / VALU_PEAK_TOPS, 4), "traffic": traffic_for_current_kernel(),
-            "kernel_ms": round(k_ms, 3), "ops_per_block": OPS_PER_BLOCK,
+            "kernel": leaf_kernel, "bound": "alu", "achieved": round(achieved, 3), "peak": round(VALU_PEAK_TOPS, 3),
+            "unit": "TOP/s", "frac": round(achieved / VALU_PEAK_TOPS, 4),
+            "traffic": traffic_for_current_kernel(alg, args.config),
+            "kernel_ms": round(k_ms, 3), "ops_per_block": ops_per_block,
             "hashed_GBps": round(total / k_ms / 1e6, 2),
-            "roof_GBps": round(VALU_PEAK_TOPS * 1e12 / OPS_PER_BLOCK * 64 / 1e9, 1),
+            "roof_GBps": round(VALU_PEAK_TOPS * 1e12 / ops_per_block * block_bytes / 1e9, 1),
         },
     }
     if not args.no_peaks:
-        valu = hv.measure_valu_peak(dev)
-        sha = hv.measure_sha256_ceiling(dev)
+        valu = hv.measure_valu_peak(dev, mix=alg)
+        sha = hv.measure_sha256_ceiling(dev, alg=alg)
         hbm = hv.measure_hbm_read(16 << 30, dev)
         kernel_blocks_per_s = blocks / (k_ms / 1e3)
-        log(f"measured peaks: VALU mix {valu['tops']:.2f} TOP/s, register-only SHA-256 "
+        log(f"measured peaks: {alg} VALU mix {valu['tops']:.2f} TOP/s, register-only {alg} "
             f"{sha['GBps_equiv']:.0f} GB/s-equiv, HBM read {hbm['GBps']:.0f} GB/s")
         line["roofline"]["measured_valu_peak"] = round(valu["tops"], 3)
         line["roofline"]["frac_of_measured_valu_peak"] = round(achieved / valu["tops"], 4)
-        line["roofline"]["register_sha256_GBps"] = round(sha["GBps_equiv"], 1)
-        line["roofline"]["frac_of_register_sha256"] = round(kernel_blocks_per_s / sha["blocks_per_s"], 4)
+        line["roofline"][f"register_{alg}_GBps"] = round(sha["GBps_equiv"], 1)
+        line["roofline"][f"frac_of_register_{alg}"] = round(kernel_blocks_per_s / sha["blocks_per_s"], 4)
         line["roofline"]["measured_hbm_read_GBps"] = round(hbm["GBps"], 1)
     if not args.no_cpu_baseline:
         log("cpu baseline ...")
-        line["cpu_baseline"] = cpu_baseline(wl, pipe, args.cpu_sample_mib << 20)
+        line["cpu_baseline"] = cpu_baseline(wl, pipe, args.cpu_sample_mib << 20, alg)
     print(json.dumps(line), flush=True)
 
 

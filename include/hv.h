@@ -61,6 +61,14 @@ typedef struct {
 
 enum { HV_DIGEST_BYTES = 32 };
 
+/* Hash of a call.  The plain entry points use SHA-256 (FIPS 180-4 6.2: 32-byte
+ * digests, 64-byte blocks).  The *_alg entry points also take SHA-384 (FIPS
+ * 180-4 6.5: 48-byte digests, 128-byte blocks) -- the hash of the paper's own
+ * kernel listings and the 48-byte digest of its C ABI (Implementation).  With
+ * SHA-384 every digest, Merkle node and root is 48 bytes, the tree is RFC 6962
+ * with SHA-384 as its hash, and chunk_bytes must be 0 or a multiple of 128. */
+typedef enum { HV_SHA256 = 0, HV_SHA384 = 1 } hv_alg;
+
 /* Leaf layout (synchronous, host only, touches no device memory).
  * Chunking (Algorithm 1): a message of L bytes with chunk size C > 0 has
  * ceil(L / C) leaves (none when L == 0); chunk i covers bytes
@@ -143,11 +151,30 @@ hv_status hv_verify_root(const uint8_t* root, const uint8_t expected[32], int* m
 hv_status hv_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32_t n,
                            uint32_t* mismatch, hipStream_t stream);
 
+/* The same four operations with an explicit hash (hv_alg).  Digest, node and
+ * root sizes are 32 bytes for HV_SHA256 and 48 for HV_SHA384 (all arrays
+ * [n][32] or [n][48]); `expected` holds that many bytes.  Semantics, layout
+ * and errors are those of the SHA-256 calls above, plus HV_ERR_INVALID_ARG
+ * for an unknown algorithm or (SHA-384) a chunk size that is not a multiple
+ * of 128.  The workspace sizes of hv_hash_workspace_bytes and
+ * hv_verify_workspace_bytes serve both hashes; hv_merkle_workspace_bytes_alg
+ * returns 0 (and sets hv_last_error) for an unknown algorithm. */
+hv_status hv_hash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                             uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, hipStream_t stream);
+size_t hv_merkle_workspace_bytes_alg(hv_alg alg, uint64_t n_nodes, uint32_t n_seg);
+hv_status hv_merkle_reduce_alg(hv_alg alg, const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg,
+                               uint8_t* roots, void* workspace, size_t workspace_bytes, hipStream_t stream);
+hv_status hv_verify_root_alg(hv_alg alg, const uint8_t* root, const uint8_t* expected, int* match, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+hv_status hv_compare_roots_alg(hv_alg alg, const uint8_t* roots, const uint8_t* expected, uint32_t n,
+                               uint32_t* mismatch, hipStream_t stream);
+
 /* Detail string for the last non-OK status returned on this thread. */
 const char* hv_last_error(void);
 
 /* Kernel timing for measurement.  When enabled (per thread), hv_hash_chunks
- * records HIP events on `stream` around its SHA-256 leaf kernel, and
+ * records HIP events on `stream` around its leaf kernel (SHA-256, or SHA-384
+ * for hv_hash_chunks_alg), and
  * hv_leaf_kernel_ms() waits for the last such pair and returns the elapsed
  * milliseconds.  Off by default; costs two event records per call when on.
  * Errors: HV_ERR_INVALID_ARG if no timed call was made on this thread. */

@@ -35,6 +35,20 @@ hv_status hv_mb_valu(uint32_t* sink, uint32_t grid, uint32_t iters, uint64_t* op
 hv_status hv_mb_sha256(uint32_t* sink, uint32_t grid, uint32_t blocks, uint64_t* blocks_per_launch,
                        hipStream_t stream);
 
+/* The SHA-384 mix (FIPS 180-4 section 6.4 on 32-bit lanes): independent
+ * chains of a 64-bit rotate (two v_alignbit_b32), a 3-input XOR of 64-bit
+ * words (two v_bitop3_b32) and a 64-bit add (one v_lshl_add_u64), `iters`
+ * trips per lane.  Its rate against hv_mb_valu's shows whether the 64-bit
+ * add issues at the 32-bit rate.  Arguments and errors as hv_mb_valu;
+ * ops_per_launch counts five instructions per chain and trip. */
+hv_status hv_mb_valu64(uint32_t* sink, uint32_t grid, uint32_t iters, uint64_t* ops_per_launch, hipStream_t stream);
+
+/* SHA-384 compressions chained on registers only (section 6.4 rounds on
+ * 1024-bit blocks, SHA-384's initial value), as hv_mb_sha256: the ceiling of
+ * the SHA-384 leaf kernel's arithmetic.  Arguments and errors as hv_mb_sha256. */
+hv_status hv_mb_sha384(uint32_t* sink, uint32_t grid, uint32_t blocks, uint64_t* blocks_per_launch,
+                       hipStream_t stream);
+
 /* Streaming read of `nbytes` (a multiple of 16) at `buf` with 16-byte loads,
  * grid-stride, folded to one word per lane.
  *   buf: device, 16-byte aligned.   sink: device, grid * 256 uint32.

@@ -189,7 +189,7 @@ def leaf_digests_mt(messages, C: int, nthreads: int, alg: str = "sha256") -> np.
     return _leaf_digests_raw(ptrs, lens, C, nthreads, alg)
 
 
-def leaf_digests_mt_packed(buf: np.ndarray, offsets, lens, C: int, nthreads: int) -> np.ndarray:
+def leaf_digests_mt_packed(buf: np.ndarray, offsets, lens, C: int, nthreads: int, alg: str = "sha256") -> np.ndarray:
     """As leaf_digests_mt for messages lying in one host buffer at byte offsets."""
     b = _as_u8(buf)
     offsets = np.asarray(offsets, dtype=np.uint64)
@@ -197,7 +197,7 @@ def leaf_digests_mt_packed(buf: np.ndarray, offsets, lens, C: int, nthreads: int
     if len(lens) and int((offsets + lens).max()) > b.size:
         raise ValueError("message range outside the buffer")
     ptrs = np.uint64(b.ctypes.data) + offsets
-    return _leaf_digests_raw(ptrs, lens, C, nthreads)
+    return _leaf_digests_raw(ptrs, lens, C, nthreads, alg)
 
 
 def _leaf_digests_raw(ptrs: np.ndarray, lens: np.ndarray, C: int, nthreads: int, alg: str = "sha256") -> np.ndarray:

@@ -106,13 +106,15 @@ uint64_t tiles_bound(uint64_t n_nodes, uint32_t n_seg) {
     return n_nodes / hv::kTileNodes + (uint64_t)n_seg + 1;
 }
 
-MerkleLayout merkle_layout(void* ws, uint64_t n_nodes, uint32_t n_seg) {
+uint32_t digest_bytes(hv_alg alg) { return alg == HV_SHA384 ? 48 : 32; }
+
+MerkleLayout merkle_layout(void* ws, uint64_t n_nodes, uint32_t n_seg, uint32_t D) {
     Carver c(ws);
     MerkleLayout L;
     L.table = c.take<uint64_t>((size_t)(kMaxLaunches + 1) * ((size_t)n_seg + 1));
     const uint64_t nb = tiles_bound(n_nodes, n_seg);
-    L.ping = c.take<uint8_t>(nb * 32);
-    L.pong = c.take<uint8_t>(nb * 32);
+    L.ping = c.take<uint8_t>(nb * D);
+    L.pong = c.take<uint8_t>(nb * D);
     L.bytes = c.used;
     return L;
 }
@@ -189,8 +191,12 @@ size_t hv_hash_workspace_bytes(uint32_t n_msgs, uint64_t n_leaves) {
     return hash_layout(nullptr, n_msgs, n_leaves).bytes;
 }
 
-hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint8_t* leaf_digests,
-                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+hv_status hv_hash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                             uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+    if (alg == HV_SHA384 && chunk_bytes % 128 != 0)
+        return fail(HV_ERR_INVALID_ARG, "chunk_bytes = %llu is not 0 or a multiple of 128 (SHA-384 blocks)",
+                    (unsigned long long)chunk_bytes);
     HashLayout L;
     uint64_t n_leaves = 0;
     hv_status st = schedule(msgs, n_msgs, chunk_bytes, true, leaf_digests, workspace, workspace_bytes, stream, &L,
@@ -204,13 +210,19 @@ hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_byt
         if (!T.stop && (e = hipEventCreate(&T.stop)) != hipSuccess) return hip_fail(e, "event create");
         if ((e = hipEventRecord(T.start, stream)) != hipSuccess) return hip_fail(e, "event record");
     }
-    if ((e = hv::launch_sha256_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream)) != hipSuccess)
-        return hip_fail(e, "sha256 leaf kernel");
+    e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream)
+                         : hv::launch_sha256_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream);
+    if (e != hipSuccess) return hip_fail(e, "leaf kernel");
     if (T.enabled) {
         if ((e = hipEventRecord(T.stop, stream)) != hipSuccess) return hip_fail(e, "event record");
         T.have = true;
     }
     return HV_OK;
+}
+
+hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint8_t* leaf_digests,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return hv_hash_chunks_alg(HV_SHA256, msgs, n_msgs, chunk_bytes, leaf_digests, workspace, workspace_bytes, stream);
 }
 
 hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t* table,
@@ -227,12 +239,22 @@ hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_b
     return HV_OK;
 }
 
-size_t hv_merkle_workspace_bytes(uint64_t n_nodes, uint32_t n_seg) {
-    return merkle_layout(nullptr, n_nodes, n_seg).bytes;
+size_t hv_merkle_workspace_bytes_alg(hv_alg alg, uint64_t n_nodes, uint32_t n_seg) {
+    if (alg != HV_SHA256 && alg != HV_SHA384) {
+        (void)fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+        return 0;
+    }
+    return merkle_layout(nullptr, n_nodes, n_seg, digest_bytes(alg)).bytes;
 }
 
-hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg, uint8_t* roots,
-                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+size_t hv_merkle_workspace_bytes(uint64_t n_nodes, uint32_t n_seg) {
+    return hv_merkle_workspace_bytes_alg(HV_SHA256, n_nodes, n_seg);
+}
+
+hv_status hv_merkle_reduce_alg(hv_alg alg, const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg,
+                               uint8_t* roots, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+    const uint32_t D = digest_bytes(alg);
     if (n_seg == 0) return fail(HV_ERR_INVALID_ARG, "n_seg is 0");
     if (seg_offsets == nullptr) return fail(HV_ERR_INVALID_ARG, "seg_offsets is NULL");
     if (roots == nullptr) return fail(HV_ERR_INVALID_ARG, "roots is NULL");
@@ -247,7 +269,7 @@ hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, ui
     if (n_nodes > 0 && nodes == nullptr) return fail(HV_ERR_INVALID_ARG, "nodes is NULL");
     if ((uintptr_t)nodes % 16 != 0 || (uintptr_t)roots % 16 != 0)
         return fail(HV_ERR_INVALID_ARG, "nodes and roots must be 16-byte aligned");
-    const MerkleLayout need = merkle_layout(nullptr, n_nodes, n_seg);
+    const MerkleLayout need = merkle_layout(nullptr, n_nodes, n_seg, D);
     if (workspace == nullptr || workspace_bytes < need.bytes)
         return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu%s", need.bytes, workspace_bytes,
                     workspace ? "" : " (NULL)");
@@ -274,7 +296,7 @@ hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, ui
         if (launches == kMaxLaunches) return fail(HV_ERR_INVALID_ARG, "tree too deep");
     }
 
-    const MerkleLayout L = merkle_layout(workspace, n_nodes, n_seg);
+    const MerkleLayout L = merkle_layout(workspace, n_nodes, n_seg, D);
     hipError_t e = hipMemcpyAsync(L.table, table.data(), table.size() * sizeof(uint64_t), hipMemcpyHostToDevice,
                                   stream);
     if (e != hipSuccess) return hip_fail(e, "plan upload");
@@ -284,25 +306,30 @@ hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, ui
         const uint64_t* in_off = L.table + (size_t)(k - 1) * row;
         const uint64_t* tile_off = L.table + (size_t)k * row;
         const uint64_t n_tiles = table[(size_t)k * row + n_seg];
-        if ((e = hv::launch_merkle_tiles(in, out, in_off, tile_off, n_seg, n_tiles, k == 1, stream)) != hipSuccess)
+        if ((e = hv::launch_merkle_tiles(alg == HV_SHA384 ? hv::kAlgSha384 : hv::kAlgSha256, in, out, in_off, tile_off,
+                                         n_seg, n_tiles, k == 1, stream)) != hipSuccess)
             return hip_fail(e, "merkle kernel");
         in = out;
     }
     return HV_OK;
 }
 
+hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg, uint8_t* roots,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return hv_merkle_reduce_alg(HV_SHA256, nodes, seg_offsets, n_seg, roots, workspace, workspace_bytes, stream);
+}
+
 size_t hv_verify_workspace_bytes(void) { return kAlign; }
 
-hv_status hv_verify_root(const uint8_t* root, const uint8_t expected[32], int* match, void* workspace,
-                         size_t workspace_bytes, hipStream_t stream) {
+hv_status hv_verify_root_alg(hv_alg alg, const uint8_t* root, const uint8_t* expected, int* match, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+    if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
     if (root == nullptr || expected == nullptr || match == nullptr)
         return fail(HV_ERR_INVALID_ARG, "root, expected and match must be non-NULL");
     if (workspace == nullptr || workspace_bytes < hv_verify_workspace_bytes())
         return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes", hv_verify_workspace_bytes());
-    uint32_t exp_le[8];
-    memcpy(exp_le, expected, 32);
     uint32_t* flag = static_cast<uint32_t*>(workspace);
-    hipError_t e = hv::launch_verify_root(root, exp_le, flag, stream);
+    hipError_t e = hv::launch_verify_root(root, expected, digest_bytes(alg), flag, stream);
     if (e != hipSuccess) return hip_fail(e, "verify kernel");
     uint32_t host_flag = 0;
     if ((e = hipMemcpyAsync(&host_flag, flag, sizeof host_flag, hipMemcpyDeviceToHost, stream)) != hipSuccess)
@@ -312,13 +339,24 @@ hv_status hv_verify_root(const uint8_t* root, const uint8_t expected[32], int* m
     return HV_OK;
 }
 
-hv_status hv_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32_t n, uint32_t* mismatch,
-                           hipStream_t stream) {
+hv_status hv_verify_root(const uint8_t* root, const uint8_t expected[32], int* match, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+    return hv_verify_root_alg(HV_SHA256, root, expected, match, workspace, workspace_bytes, stream);
+}
+
+hv_status hv_compare_roots_alg(hv_alg alg, const uint8_t* roots, const uint8_t* expected, uint32_t n,
+                               uint32_t* mismatch, hipStream_t stream) {
+    if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
     if (n > 0 && (roots == nullptr || expected == nullptr || mismatch == nullptr))
         return fail(HV_ERR_INVALID_ARG, "roots, expected and mismatch must be non-NULL");
-    hipError_t e = hv::launch_compare_roots(roots, expected, n, mismatch, stream);
+    hipError_t e = hv::launch_compare_roots(roots, expected, n, digest_bytes(alg), mismatch, stream);
     if (e != hipSuccess) return hip_fail(e, "compare kernel");
     return HV_OK;
+}
+
+hv_status hv_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32_t n, uint32_t* mismatch,
+                           hipStream_t stream) {
+    return hv_compare_roots_alg(HV_SHA256, roots, expected, n, mismatch, stream);
 }
 
 hv_status hv_set_kernel_timing(int enable) {

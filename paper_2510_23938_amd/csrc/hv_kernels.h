@@ -8,6 +8,11 @@
 
 namespace hv {
 
+// Hash algorithm of a call: SHA-256 (32-byte digests, 64-byte blocks) or
+// SHA-384 (48-byte digests, 128-byte blocks).
+constexpr int kAlgSha256 = 0;
+constexpr int kAlgSha384 = 1;
+
 // One leaf as the hash kernel sees it.
 struct LeafDesc {
     uint64_t src;     // device address of the chunk's first byte
@@ -36,6 +41,11 @@ hipError_t launch_sched_full(const MsgDesc* msgs, const Pair* off, uint32_t n, u
 hipError_t launch_sched_tails(const MsgDesc* msgs, const Pair* off, uint32_t n, uint64_t C, uint64_t n_full,
                               uint64_t* hist, LeafDesc* desc, hipStream_t s);
 
+// SHA-384 of the n_slots leaves of a leaf table (sha384_leaves.hip): 48-byte
+// digests at digests + 48 * desc.out for desc.out < out_bound.
+hipError_t launch_sha384_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
+                                hipStream_t s);
+
 // Leaf table for a sorted list of leaf numbers (sched.hip): desc[e] is leaf
 // leaves[e], located through the per-message offsets `off` (first leaf of
 // message m = off[m].x + off[m].y).
@@ -52,8 +62,9 @@ hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t
 // one segment and writes one node.
 constexpr int kTileLevels = 9;
 constexpr int kTileNodes = 1 << kTileLevels;
-hipError_t launch_merkle_tiles(const uint8_t* in, uint8_t* out, const uint64_t* in_off, const uint64_t* tile_off,
-                               uint32_t n_seg, uint64_t n_tiles, int leaf_mode, hipStream_t s);
+hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
+                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode,
+                               hipStream_t s);
 
 // Persistent tree for incremental updates (tree.hip).
 hipError_t launch_tree_leaf_level(const uint8_t* digests, uint64_t n, uint8_t* level0, hipStream_t s);
@@ -70,8 +81,10 @@ hipError_t launch_tree_roots(const uint8_t* top, const uint64_t* top_off, uint32
                              hipStream_t s);
 
 // Verification (verify.hip).
-hipError_t launch_verify_root(const uint8_t* root, const uint32_t expected_le[8], uint32_t* flag, hipStream_t s);
-hipError_t launch_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32_t n, uint32_t* mismatch,
-                                hipStream_t s);
+// nbytes: 32 or 48 (the digest size of the call's hash).
+hipError_t launch_verify_root(const uint8_t* root, const uint8_t* expected, uint32_t nbytes, uint32_t* flag,
+                              hipStream_t s);
+hipError_t launch_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32_t n, uint32_t nbytes,
+                                uint32_t* mismatch, hipStream_t s);
 
 }  // namespace hv

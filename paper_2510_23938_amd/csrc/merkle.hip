@@ -17,55 +17,130 @@
 // hashes as it loads the entries.  Level 1 is formed in registers from the
 // two entries a thread loads; higher levels go through LDS, with idle waves
 // waiting at the barriers.
+//
+// The kernel is written once over a node-hash policy: SHA-256 (32-byte nodes;
+// an interior node is two blocks) or SHA-384 (48-byte nodes; leaf and
+// interior nodes are one 128-byte block each).
 #include "hv_kernels.h"
 #include "sha256_device.h"
+#include "sha384_device.h"
 
 namespace hv {
 namespace {
 
 constexpr int kThreads = kTileNodes / 2;  // 256: each thread owns one pair of level 0
 
-// SHA-256(0x00 || d): 33 bytes, one block.  d as big-endian words.
-__device__ __forceinline__ void leaf_hash(const uint32_t d[8], uint32_t out[8]) {
-    uint32_t W[16];
-    W[0] = d[0] >> 8;
-#pragma unroll
-    for (int i = 1; i < 8; ++i) W[i] = (d[i - 1] << 24) | (d[i] >> 8);
-    W[8] = (d[7] << 24) | 0x00800000u;
-#pragma unroll
-    for (int i = 9; i < 15; ++i) W[i] = 0;
-    W[15] = 33 * 8;
-    init_state(out);
-    compress(out, W);
-}
+// Node hashes are held as big-endian 32-bit words: 8 for SHA-256, 12 for SHA-384.
 
-// SHA-256(0x01 || L || R): 65 bytes, two blocks.
-__device__ __forceinline__ void node_hash(const uint32_t L[8], const uint32_t R[8], uint32_t out[8]) {
-    uint32_t W[16];
-    W[0] = 0x01000000u | (L[0] >> 8);
+struct Sha256Tree {
+    static constexpr int kWords = 8;
+    static constexpr int kBytes = 32;
+    // SHA-256(0x00 || d): 33 bytes, one block.  d as big-endian words.
+    static __device__ __forceinline__ void leaf_hash(const uint32_t d[8], uint32_t out[8]) {
+        uint32_t W[16];
+        W[0] = d[0] >> 8;
 #pragma unroll
-    for (int i = 1; i < 8; ++i) W[i] = (L[i - 1] << 24) | (L[i] >> 8);
-    W[8] = (L[7] << 24) | (R[0] >> 8);
+        for (int i = 1; i < 8; ++i) W[i] = (d[i - 1] << 24) | (d[i] >> 8);
+        W[8] = (d[7] << 24) | 0x00800000u;
 #pragma unroll
-    for (int i = 1; i < 8; ++i) W[8 + i] = (R[i - 1] << 24) | (R[i] >> 8);
-    init_state(out);
-    compress(out, W);
-    W[0] = (R[7] << 24) | 0x00800000u;
-#pragma unroll
-    for (int i = 1; i < 15; ++i) W[i] = 0;
-    W[15] = 65 * 8;
-    compress(out, W);
-}
+        for (int i = 9; i < 15; ++i) W[i] = 0;
+        W[15] = 33 * 8;
+        init_state(out);
+        compress(out, W);
+    }
 
-// SHA-256 of the empty string: the root of an empty segment.
-__device__ __forceinline__ void empty_hash(uint32_t out[8]) {
-    uint32_t W[16];
-    W[0] = 0x80000000u;
+    // SHA-256(0x01 || L || R): 65 bytes, two blocks.
+    static __device__ __forceinline__ void node_hash(const uint32_t L[8], const uint32_t R[8], uint32_t out[8]) {
+        uint32_t W[16];
+        W[0] = 0x01000000u | (L[0] >> 8);
 #pragma unroll
-    for (int i = 1; i < 16; ++i) W[i] = 0;
-    init_state(out);
-    compress(out, W);
-}
+        for (int i = 1; i < 8; ++i) W[i] = (L[i - 1] << 24) | (L[i] >> 8);
+        W[8] = (L[7] << 24) | (R[0] >> 8);
+#pragma unroll
+        for (int i = 1; i < 8; ++i) W[8 + i] = (R[i - 1] << 24) | (R[i] >> 8);
+        init_state(out);
+        compress(out, W);
+        W[0] = (R[7] << 24) | 0x00800000u;
+#pragma unroll
+        for (int i = 1; i < 15; ++i) W[i] = 0;
+        W[15] = 65 * 8;
+        compress(out, W);
+    }
+
+    // SHA-256 of the empty string: the root of an empty segment.
+    static __device__ __forceinline__ void empty_hash(uint32_t out[8]) {
+        uint32_t W[16];
+        W[0] = 0x80000000u;
+#pragma unroll
+        for (int i = 1; i < 16; ++i) W[i] = 0;
+        init_state(out);
+        compress(out, W);
+    }
+
+    static __device__ __forceinline__ void load(const uint8_t* p, uint32_t D[8]) { load_digest(p, D); }
+    static __device__ __forceinline__ void store(uint8_t* p, const uint32_t D[8]) { store_digest(p, D); }
+};
+
+// SHA-384 nodes (48 bytes): both SHA-384(0x00 || d) (49 bytes) and
+// SHA-384(0x01 || L || R) (97 bytes) fit in one 128-byte block.
+struct Sha384Tree {
+    static constexpr int kWords = 12;
+    static constexpr int kBytes = 48;
+    // One block from 26 big-endian message words (the rest zero) and the bit
+    // length of `len` bytes; the state's first six words as 12 digest words.
+    static __device__ __forceinline__ void one_block(const uint32_t w32[26], uint32_t len, uint32_t out[12]) {
+        uint64_t W[16];
+#pragma unroll
+        for (int k = 0; k < 13; ++k) W[k] = pack(w32[2 * k], w32[2 * k + 1]);
+        W[13] = 0;
+        W[14] = 0;
+        W[15] = (uint64_t)len * 8;
+        uint64_t H[8];
+        init_state384(H);
+        compress512(H, W);
+#pragma unroll
+        for (int i = 0; i < 6; ++i) {
+            out[2 * i] = hi32(H[i]);
+            out[2 * i + 1] = lo32(H[i]);
+        }
+    }
+    static __device__ __forceinline__ void leaf_hash(const uint32_t d[12], uint32_t out[12]) {
+        uint32_t w[26];
+        w[0] = d[0] >> 8;
+#pragma unroll
+        for (int i = 1; i < 12; ++i) w[i] = (d[i - 1] << 24) | (d[i] >> 8);
+        w[12] = (d[11] << 24) | 0x00800000u;
+#pragma unroll
+        for (int i = 13; i < 26; ++i) w[i] = 0;
+        one_block(w, 49, out);
+    }
+    static __device__ __forceinline__ void node_hash(const uint32_t L[12], const uint32_t R[12], uint32_t out[12]) {
+        uint32_t w[26];
+        w[0] = 0x01000000u | (L[0] >> 8);
+#pragma unroll
+        for (int i = 1; i < 12; ++i) w[i] = (L[i - 1] << 24) | (L[i] >> 8);
+        w[12] = (L[11] << 24) | (R[0] >> 8);
+#pragma unroll
+        for (int i = 1; i < 12; ++i) w[12 + i] = (R[i - 1] << 24) | (R[i] >> 8);
+        w[24] = (R[11] << 24) | 0x00800000u;
+        w[25] = 0;
+        one_block(w, 97, out);
+    }
+    static __device__ __forceinline__ void empty_hash(uint32_t out[12]) {
+        uint32_t w[26];
+        w[0] = 0x80000000u;
+#pragma unroll
+        for (int i = 1; i < 26; ++i) w[i] = 0;
+        one_block(w, 0, out);
+    }
+    static __device__ __forceinline__ void load(const uint8_t* p, uint32_t D[12]) { load_digest384(p, D); }
+    static __device__ __forceinline__ void store(uint8_t* p, const uint32_t D[12]) {
+        uint4* q = reinterpret_cast<uint4*>(p);
+#pragma unroll
+        for (int i = 0; i < 3; ++i)
+            q[i] = make_uint4(bswap(D[4 * i]), bswap(D[4 * i + 1]), bswap(D[4 * i + 2]), bswap(D[4 * i + 3]));
+    }
+};
 
 __device__ __forceinline__ uint32_t find_segment(const uint64_t* __restrict__ tile_off, uint32_t n_seg, uint64_t tile) {
     uint32_t lo = 0, hi = n_seg;  // tile_off[lo] <= tile < tile_off[hi]
@@ -76,11 +151,14 @@ __device__ __forceinline__ uint32_t find_segment(const uint64_t* __restrict__ ti
     return lo;
 }
 
+template <class T>
 __global__ void __launch_bounds__(kThreads) merkle_tile_kernel(const uint8_t* __restrict__ in, uint8_t* __restrict__ out,
                                                                const uint64_t* __restrict__ in_off,
                                                                const uint64_t* __restrict__ tile_off, uint32_t n_seg,
                                                                uint64_t n_tiles, int leaf_mode) {
-    __shared__ uint32_t lds[8][kThreads];  // word-major: node i's word w at lds[w][i]
+    constexpr int NW = T::kWords;
+    constexpr int NB = T::kBytes;
+    __shared__ uint32_t lds[NW][kThreads];  // word-major: node i's word w at lds[w][i]
     const uint32_t i = threadIdx.x;
     for (uint64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
         const uint32_t s = find_segment(tile_off, n_seg, tile);
@@ -88,53 +166,53 @@ __global__ void __launch_bounds__(kThreads) merkle_tile_kernel(const uint8_t* __
         const uint64_t c = in_off[s + 1] - in_off[s];
         const uint64_t first = t * kTileNodes;
         const uint32_t cnt = c > first ? (uint32_t)(c - first < (uint64_t)kTileNodes ? c - first : kTileNodes) : 0u;
-        const uint8_t* base = in + 32 * (in_off[s] + first);
+        const uint8_t* base = in + NB * (in_off[s] + first);
 
-        uint32_t P[8];
+        uint32_t P[NW];
         uint32_t n;  // nodes held in lds after the first level
         if (cnt == 0) {  // empty segment (only ever a first-launch tile)
-            if (i == 0) empty_hash(P);
+            if (i == 0) T::empty_hash(P);
             n = 1;
         } else {
             const bool hasA = 2 * i < cnt, hasB = 2 * i + 1 < cnt;
-            uint32_t A[8], B[8];
+            uint32_t A[NW], B[NW];
             if (hasA) {
-                load_digest(base + 64 * i, A);
-                if (leaf_mode) { uint32_t T[8]; leaf_hash(A, T); for (int w = 0; w < 8; ++w) A[w] = T[w]; }
+                T::load(base + 2 * NB * i, A);
+                if (leaf_mode) { uint32_t X[NW]; T::leaf_hash(A, X); for (int w = 0; w < NW; ++w) A[w] = X[w]; }
             }
             if (hasB) {
-                load_digest(base + 64 * i + 32, B);
-                if (leaf_mode) { uint32_t T[8]; leaf_hash(B, T); for (int w = 0; w < 8; ++w) B[w] = T[w]; }
-                node_hash(A, B, P);
+                T::load(base + 2 * NB * i + NB, B);
+                if (leaf_mode) { uint32_t X[NW]; T::leaf_hash(B, X); for (int w = 0; w < NW; ++w) B[w] = X[w]; }
+                T::node_hash(A, B, P);
             } else if (hasA) {
-                for (int w = 0; w < 8; ++w) P[w] = A[w];  // unpaired last node moves up
+                for (int w = 0; w < NW; ++w) P[w] = A[w];  // unpaired last node moves up
             }
             n = (cnt + 1) / 2;
         }
-        if (i < n) for (int w = 0; w < 8; ++w) lds[w][i] = P[w];
+        if (i < n) for (int w = 0; w < NW; ++w) lds[w][i] = P[w];
         __syncthreads();
         while (n > 1) {
             const uint32_t m = (n + 1) / 2;
             if (i < m) {
-                uint32_t L[8];
-                for (int w = 0; w < 8; ++w) L[w] = lds[w][2 * i];
+                uint32_t L[NW];
+                for (int w = 0; w < NW; ++w) L[w] = lds[w][2 * i];
                 if (2 * i + 1 < n) {
-                    uint32_t R[8];
-                    for (int w = 0; w < 8; ++w) R[w] = lds[w][2 * i + 1];
-                    node_hash(L, R, P);
+                    uint32_t R[NW];
+                    for (int w = 0; w < NW; ++w) R[w] = lds[w][2 * i + 1];
+                    T::node_hash(L, R, P);
                 } else {
-                    for (int w = 0; w < 8; ++w) P[w] = L[w];
+                    for (int w = 0; w < NW; ++w) P[w] = L[w];
                 }
             }
             __syncthreads();
-            if (i < m) for (int w = 0; w < 8; ++w) lds[w][i] = P[w];
+            if (i < m) for (int w = 0; w < NW; ++w) lds[w][i] = P[w];
             __syncthreads();
             n = m;
         }
         if (i == 0) {
-            uint32_t R[8];
-            for (int w = 0; w < 8; ++w) R[w] = lds[w][0];
-            store_digest(out + 32 * tile, R);
+            uint32_t R[NW];
+            for (int w = 0; w < NW; ++w) R[w] = lds[w][0];
+            T::store(out + NB * tile, R);
         }
         __syncthreads();  // lds is reused by the next tile
     }
@@ -142,12 +220,16 @@ __global__ void __launch_bounds__(kThreads) merkle_tile_kernel(const uint8_t* __
 
 }  // namespace
 
-hipError_t launch_merkle_tiles(const uint8_t* in, uint8_t* out, const uint64_t* in_off, const uint64_t* tile_off,
-                               uint32_t n_seg, uint64_t n_tiles, int leaf_mode, hipStream_t s) {
+hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
+                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode,
+                               hipStream_t s) {
     if (n_tiles == 0) return hipSuccess;
     const uint64_t cap = 1u << 20;
     const unsigned grid = (unsigned)(n_tiles < cap ? n_tiles : cap);
-    merkle_tile_kernel<<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
+    if (alg == kAlgSha384)
+        merkle_tile_kernel<Sha384Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
+    else
+        merkle_tile_kernel<Sha256Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
     return hipGetLastError();
 }
 

@@ -1,10 +1,13 @@
 // microbench.hip -- roofline denominators measured on the device: the issue
-// rate of the SHA-256 VALU mix and the streaming HBM read bandwidth.
+// rate of the SHA-256 VALU mix and of the SHA-384 mix (32-bit logic on word
+// halves plus 64-bit adds), register-only SHA-256 / SHA-384 ceilings, and the
+// streaming HBM read bandwidth.
 #include <hip/hip_runtime.h>
 
 #include "hv.h"
 #include "hv_microbench.h"
 #include "sha256_device.h"
+#include "sha384_device.h"
 
 namespace {
 
@@ -31,6 +34,33 @@ __global__ void __launch_bounds__(kThreads) valu_mix_kernel(uint32_t* __restrict
     uint32_t r = 0;
 #pragma unroll
     for (int k = 0; k < kChains; ++k) r ^= x[k];
+    sink[tid] = r;
+}
+
+// The SHA-384 round mix: per chain and trip, a 64-bit rotate (two
+// v_alignbit_b32), a 3-input XOR on both halves (two v_bitop3_b32) and one
+// 64-bit add (v_lshl_add_u64): five instructions.
+constexpr int kOpsPerChain64 = 5;
+
+__global__ void __launch_bounds__(kThreads) valu64_mix_kernel(uint32_t* __restrict__ sink, uint32_t iters,
+                                                              uint32_t seed) {
+    const uint32_t tid = blockIdx.x * kThreads + threadIdx.x;
+    uint64_t x[kChains];
+#pragma unroll
+    for (int k = 0; k < kChains; ++k)
+        x[k] = hv::pack(seed ^ (tid * 0x9E3779B9u), (uint32_t)(k * 0x85EBCA6Bu) + tid);
+    const uint64_t y = hv::pack(tid ^ seed, tid + seed), z = hv::pack(tid * 3u, seed ^ 0x5bd1e995u);
+#pragma unroll 4
+    for (uint32_t it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int k = 0; k < kChains; ++k) {
+            const uint64_t a = hv::rotr64<7>(x[k]);
+            x[k] = hv::bitop3_64<0x96>(a, y, z) + x[k];
+        }
+    }
+    uint32_t r = 0;
+#pragma unroll
+    for (int k = 0; k < kChains; ++k) r ^= hv::hi32(x[k]) ^ hv::lo32(x[k]);
     sink[tid] = r;
 }
 
@@ -73,6 +103,26 @@ __global__ void __launch_bounds__(kThreads) sha256_registers_kernel(uint32_t* __
     sink[tid] = r;
 }
 
+// SHA-384 compressions on registers only (section 6.4 rounds), as above.
+__global__ void __launch_bounds__(kThreads) sha384_registers_kernel(uint32_t* __restrict__ sink, uint32_t blocks) {
+    const uint32_t tid = blockIdx.x * kThreads + threadIdx.x;
+    uint64_t H[8];
+    hv::init_state384(H);
+    uint64_t M[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) M[i] = hv::pack(tid, (uint32_t)i);
+    for (uint32_t b = 0; b < blocks; ++b) {
+        uint64_t W[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) W[i] = M[i] ^ H[i & 7];
+        hv::compress512(H, W);
+    }
+    uint32_t r = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r ^= hv::hi32(H[i]) ^ hv::lo32(H[i]);
+    sink[tid] = r;
+}
+
 }  // namespace
 
 extern "C" {
@@ -88,6 +138,21 @@ hv_status hv_mb_sha256(uint32_t* sink, uint32_t grid, uint32_t blocks, uint64_t*
                        hipStream_t stream) {
     if (sink == nullptr || blocks_per_launch == nullptr || grid == 0) return HV_ERR_INVALID_ARG;
     sha256_registers_kernel<<<grid, kThreads, 0, stream>>>(sink, blocks);
+    *blocks_per_launch = (uint64_t)grid * kThreads * blocks;
+    return hipGetLastError() == hipSuccess ? HV_OK : HV_ERR_HIP;
+}
+
+hv_status hv_mb_valu64(uint32_t* sink, uint32_t grid, uint32_t iters, uint64_t* ops_per_launch, hipStream_t stream) {
+    if (sink == nullptr || ops_per_launch == nullptr || grid == 0) return HV_ERR_INVALID_ARG;
+    valu64_mix_kernel<<<grid, kThreads, 0, stream>>>(sink, iters, 0x2510u);
+    *ops_per_launch = (uint64_t)grid * kThreads * iters * kChains * kOpsPerChain64;
+    return hipGetLastError() == hipSuccess ? HV_OK : HV_ERR_HIP;
+}
+
+hv_status hv_mb_sha384(uint32_t* sink, uint32_t grid, uint32_t blocks, uint64_t* blocks_per_launch,
+                       hipStream_t stream) {
+    if (sink == nullptr || blocks_per_launch == nullptr || grid == 0) return HV_ERR_INVALID_ARG;
+    sha384_registers_kernel<<<grid, kThreads, 0, stream>>>(sink, blocks);
     *blocks_per_launch = (uint64_t)grid * kThreads * blocks;
     return hipGetLastError() == hipSuccess ? HV_OK : HV_ERR_HIP;
 }

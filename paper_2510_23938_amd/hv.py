@@ -15,6 +15,9 @@ Names follow the C ABI:
 * ``hv_verify_root(root, expected)``       -> bool
 * ``hv_compare_roots(roots, expected)``    -> mismatch flags [n] (int32)
 
+Each of the four takes ``alg="sha256"`` (default; 32-byte digests) or
+``alg="sha384"`` (48-byte digests, the ``*_alg`` entry points).
+
 plus compositions used by callers: ``manifest_root`` (per-tensor roots, then
 one root over them in the given order -- the paper's hierarchical roots) and
 ``verify`` (raises ``VerificationError`` on a mismatch, as the paper's
@@ -32,15 +35,19 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhv.so")
 
 HV_OK, HV_ERR_INVALID_ARG, HV_ERR_WORKSPACE, HV_ERR_HIP = 0, 1, 2, 3
+HV_SHA256, HV_SHA384 = 0, 1
+# hash name -> (hv_alg code, digest bytes)
+ALGS = {"sha256": (HV_SHA256, 32), "sha384": (HV_SHA384, 48)}
 _STATUS = {1: "HV_ERR_INVALID_ARG", 2: "HV_ERR_WORKSPACE", 3: "HV_ERR_HIP"}
 
 # exported symbols, in the order include/hv.h declares them
 EXPORTS = (
     "hv_leaf_layout", "hv_hash_workspace_bytes", "hv_hash_chunks", "hv_merkle_workspace_bytes",
     "hv_merkle_reduce", "hv_verify_workspace_bytes", "hv_verify_root", "hv_compare_roots",
-    "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
+    "hv_hash_chunks_alg", "hv_merkle_workspace_bytes_alg", "hv_merkle_reduce_alg", "hv_verify_root_alg",
+    "hv_compare_roots_alg", "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
     "hv_leaf_schedule",  # include/hv_inspect.h
-    "hv_mb_valu", "hv_mb_sha256", "hv_mb_hbm_read",  # include/hv_microbench.h
+    "hv_mb_valu", "hv_mb_sha256", "hv_mb_valu64", "hv_mb_sha384", "hv_mb_hbm_read",  # include/hv_microbench.h
     "hv_stream_workspace_bytes", "hv_hash_host_chunks",  # include/hv_stream.h
     "hv_tree_bytes", "hv_tree_build", "hv_tree_update_workspace_bytes", "hv_tree_update",
     "hv_rehash_workspace_bytes", "hv_rehash_chunks",  # include/hv_incremental.h
@@ -77,6 +84,11 @@ def _load():
         "hv_verify_workspace_bytes": ([], sz),
         "hv_verify_root": ([vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "hv_compare_roots": ([vp, vp, u32, vp, vp], ctypes.c_int),
+        "hv_hash_chunks_alg": ([ctypes.c_int, vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
+        "hv_merkle_workspace_bytes_alg": ([ctypes.c_int, u64, u32], sz),
+        "hv_merkle_reduce_alg": ([ctypes.c_int, vp, vp, u32, vp, vp, sz, vp], ctypes.c_int),
+        "hv_verify_root_alg": ([ctypes.c_int, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "hv_compare_roots_alg": ([ctypes.c_int, vp, vp, u32, vp, vp], ctypes.c_int),
         "hv_last_error": ([], ctypes.c_char_p),
         "hv_set_kernel_timing": ([ctypes.c_int], ctypes.c_int),
         "hv_leaf_kernel_ms": ([vp], ctypes.c_int),
@@ -84,6 +96,8 @@ def _load():
         "hv_mb_valu": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_hbm_read": ([vp, u64, vp, u32, vp], ctypes.c_int),
         "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
+        "hv_mb_valu64": ([vp, u32, u32, vp, vp], ctypes.c_int),
+        "hv_mb_sha384": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_stream_workspace_bytes": ([vp, u32, u64, u64], sz),
         "hv_hash_host_chunks": ([vp, u32, u64, vp, u64, vp, sz, vp, vp], ctypes.c_int),
         "hv_tree_bytes": ([vp, u32], sz),
@@ -105,6 +119,14 @@ lib = _load()
 def _check(status: int):
     if status != HV_OK:
         raise HVError(status, lib.hv_last_error().decode("utf-8", "replace"))
+
+
+def _alg(alg: str) -> tuple:
+    """(hv_alg code, digest bytes) of a hash name."""
+    try:
+        return ALGS[alg]
+    except KeyError:
+        raise ValueError(f"unknown hash {alg!r}; expected one of {sorted(ALGS)}") from None
 
 
 def _stream(device=None) -> int:
@@ -162,19 +184,42 @@ def hv_leaf_layout(ptrs, lens, chunk_bytes: int):
     return seg, int(n_leaves.value)
 
 
-def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace | None = None, out=None):
+def _hash_call(alg: str, arr, n, chunk_bytes, out_ptr, ws, stream):
+    code, _ = _alg(alg)
+    if code == HV_SHA256:
+        return lib.hv_hash_chunks(arr, n, chunk_bytes, out_ptr, ws.data_ptr(), ws.numel(), stream)
+    return lib.hv_hash_chunks_alg(code, arr, n, chunk_bytes, out_ptr, ws.data_ptr(), ws.numel(), stream)
+
+
+def _merkle_call(alg: str, nodes_ptr, seg_ptr, n_seg, roots_ptr, ws, stream):
+    code, _ = _alg(alg)
+    if code == HV_SHA256:
+        return lib.hv_merkle_reduce(nodes_ptr, seg_ptr, n_seg, roots_ptr, ws.data_ptr(), ws.numel(), stream)
+    return lib.hv_merkle_reduce_alg(code, nodes_ptr, seg_ptr, n_seg, roots_ptr, ws.data_ptr(), ws.numel(), stream)
+
+
+def _merkle_ws_bytes(alg: str, n_nodes: int, n_seg: int) -> int:
+    code, _ = _alg(alg)
+    if code == HV_SHA256:
+        return lib.hv_merkle_workspace_bytes(n_nodes, n_seg)
+    return lib.hv_merkle_workspace_bytes_alg(code, n_nodes, n_seg)
+
+
+def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace | None = None, out=None,
+                   alg: str = "sha256"):
     """Leaf digests of ``msgs`` (tensors, a (ptrs, lens) pair, or an object with
-    ``ptrs``/``lens``): ([n_leaves, 32] uint8 device tensor, seg_offsets)."""
+    ``ptrs``/``lens``): ([n_leaves, D] uint8 device tensor, seg_offsets), D the digest size."""
+    _, D = _alg(alg)
     ptrs, lens = _ptr_len(msgs)
     seg, n_leaves = hv_leaf_layout(ptrs, lens, chunk_bytes)
     arr = _msg_array(ptrs, lens)
     n = len(arr)
     dev = torch.device(device)
     if out is None:
-        out = torch.empty((n_leaves, 32), dtype=torch.uint8, device=dev)
+        out = torch.empty((n_leaves, D), dtype=torch.uint8, device=dev)
     ws = (workspace or Workspace(dev)).get(lib.hv_hash_workspace_bytes(n, n_leaves))
-    _check(lib.hv_hash_chunks(arr.ctypes.data if n else None, n, chunk_bytes, out.data_ptr() if n_leaves else None,
-                              ws.data_ptr(), ws.numel(), _stream(dev)))
+    _check(_hash_call(alg, arr.ctypes.data if n else None, n, chunk_bytes, out.data_ptr() if n_leaves else None, ws,
+                      _stream(dev)))
     return out, seg
 
 
@@ -215,34 +260,53 @@ def hv_hash_host_chunks(host_msgs, chunk_bytes: int, batch_bytes: int = 1 << 30,
     return out, seg
 
 
-def hv_merkle_reduce(nodes: torch.Tensor, seg_offsets, workspace: Workspace | None = None, out=None):
-    """Per-segment RFC 6962 roots of ``nodes`` ([n, 32] uint8 device tensor)."""
+def hv_merkle_reduce(nodes: torch.Tensor, seg_offsets, workspace: Workspace | None = None, out=None,
+                     alg: str = "sha256"):
+    """Per-segment RFC 6962 roots of ``nodes`` ([n, D] uint8 device tensor, D the digest size)."""
+    _, D = _alg(alg)
     seg = np.ascontiguousarray(seg_offsets, dtype=np.uint64)
     n_seg = len(seg) - 1
     if out is None:
-        out = torch.empty((max(n_seg, 0), 32), dtype=torch.uint8, device=nodes.device)
-    ws = (workspace or Workspace(nodes.device)).get(lib.hv_merkle_workspace_bytes(int(seg[-1]), n_seg))
-    _check(lib.hv_merkle_reduce(nodes.data_ptr() if nodes.numel() else None, seg.ctypes.data, n_seg,
-                                out.data_ptr() if n_seg else None, ws.data_ptr(), ws.numel(),
-                                _stream(nodes.device)))
+        out = torch.empty((max(n_seg, 0), D), dtype=torch.uint8, device=nodes.device)
+    ws = (workspace or Workspace(nodes.device)).get(_merkle_ws_bytes(alg, int(seg[-1]), n_seg))
+    _check(_merkle_call(alg, nodes.data_ptr() if nodes.numel() else None, seg.ctypes.data, n_seg,
+                        out.data_ptr() if n_seg else None, ws, _stream(nodes.device)))
     return out
 
 
-def hv_verify_root(root: torch.Tensor, expected: bytes, workspace: Workspace | None = None) -> bool:
-    """The 32 device bytes of ``root`` equal ``expected`` (compared on the GPU)."""
-    exp = (ctypes.c_uint8 * 32).from_buffer_copy(bytes(expected))
+def hv_verify_root(root: torch.Tensor, expected: bytes, workspace: Workspace | None = None,
+                   alg: str = "sha256") -> bool:
+    """The D device bytes of ``root`` equal ``expected`` (compared on the GPU; D the digest size)."""
+    code, D = _alg(alg)
+    expected = bytes(expected)
+    if len(expected) != D:
+        raise ValueError(f"expected root must be {D} bytes for {alg}, got {len(expected)}")
+    exp = (ctypes.c_uint8 * D).from_buffer_copy(expected)
     match = ctypes.c_int(-1)
     ws = (workspace or Workspace(root.device)).get(lib.hv_verify_workspace_bytes())
-    _check(lib.hv_verify_root(root.data_ptr(), exp, ctypes.byref(match), ws.data_ptr(), ws.numel(),
-                              _stream(root.device)))
+    if code == HV_SHA256:
+        st = lib.hv_verify_root(root.data_ptr(), exp, ctypes.byref(match), ws.data_ptr(), ws.numel(),
+                                _stream(root.device))
+    else:
+        st = lib.hv_verify_root_alg(code, root.data_ptr(), exp, ctypes.byref(match), ws.data_ptr(), ws.numel(),
+                                    _stream(root.device))
+    _check(st)
     return match.value == 1
 
 
-def hv_compare_roots(roots: torch.Tensor, expected: torch.Tensor) -> torch.Tensor:
-    """int32 [n]: 1 where roots[i] differs from expected[i] (both [n, 32] device)."""
+def hv_compare_roots(roots: torch.Tensor, expected: torch.Tensor, alg: str = "sha256") -> torch.Tensor:
+    """int32 [n]: 1 where roots[i] differs from expected[i] (both [n, D] device)."""
+    code, D = _alg(alg)
     n = roots.shape[0]
+    if roots.shape != (n, D) or expected.shape != (n, D):
+        raise ValueError(f"roots and expected must both be [n, {D}] for {alg}")
     mism = torch.empty(n, dtype=torch.int32, device=roots.device)
-    _check(lib.hv_compare_roots(roots.data_ptr(), expected.data_ptr(), n, mism.data_ptr(), _stream(roots.device)))
+    if code == HV_SHA256:
+        st = lib.hv_compare_roots(roots.data_ptr(), expected.data_ptr(), n, mism.data_ptr(), _stream(roots.device))
+    else:
+        st = lib.hv_compare_roots_alg(code, roots.data_ptr(), expected.data_ptr(), n, mism.data_ptr(),
+                                      _stream(roots.device))
+    _check(st)
     return mism
 
 
@@ -261,18 +325,20 @@ def hv_leaf_schedule(msgs, chunk_bytes: int, device="cuda") -> np.ndarray:
     return table
 
 
-def measure_valu_peak(device="cuda", grid=16384, iters=4096, reps=5) -> dict:
-    """Best rate of the SHA-256 VALU mix (alignbit / bitop3 / add3) over reps launches."""
+def measure_valu_peak(device="cuda", grid=16384, iters=4096, reps=5, mix: str = "sha256") -> dict:
+    """Best rate of a hash's VALU mix over reps launches: "sha256" (alignbit /
+    bitop3 / add3) or "sha384" (the same logic on word halves plus 64-bit adds)."""
+    fn = {"sha256": lib.hv_mb_valu, "sha384": lib.hv_mb_valu64}[mix]
     dev = torch.device(device)
     sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
     ops = ctypes.c_uint64(0)
     s = _stream(dev)
-    _check(lib.hv_mb_valu(sink.data_ptr(), grid, 64, ctypes.byref(ops), s))  # warm-up
+    _check(fn(sink.data_ptr(), grid, 64, ctypes.byref(ops), s))  # warm-up
     best = None
     for _ in range(reps):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
-        _check(lib.hv_mb_valu(sink.data_ptr(), grid, iters, ctypes.byref(ops), s))
+        _check(fn(sink.data_ptr(), grid, iters, ctypes.byref(ops), s))
         b.record()
         b.synchronize()
         ms = a.elapsed_time(b)
@@ -280,24 +346,26 @@ def measure_valu_peak(device="cuda", grid=16384, iters=4096, reps=5) -> dict:
     return {"tops": ops.value / (best / 1e3) / 1e12, "ms": best, "ops": ops.value, "grid": grid, "iters": iters}
 
 
-def measure_sha256_ceiling(device="cuda", grid=8192, blocks=256, reps=5) -> dict:
-    """Best rate of register-only SHA-256 compressions (no memory traffic)."""
+def measure_sha256_ceiling(device="cuda", grid=8192, blocks=256, reps=5, alg: str = "sha256") -> dict:
+    """Best rate of register-only compressions (no memory traffic) of a hash:
+    64-byte SHA-256 blocks, or 128-byte SHA-384 blocks with alg="sha384"."""
+    fn, block_bytes = {"sha256": (lib.hv_mb_sha256, 64), "sha384": (lib.hv_mb_sha384, 128)}[alg]
     dev = torch.device(device)
     sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
     n = ctypes.c_uint64(0)
     s = _stream(dev)
-    _check(lib.hv_mb_sha256(sink.data_ptr(), grid, 8, ctypes.byref(n), s))  # warm-up
+    _check(fn(sink.data_ptr(), grid, 8, ctypes.byref(n), s))  # warm-up
     best = None
     for _ in range(reps):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
-        _check(lib.hv_mb_sha256(sink.data_ptr(), grid, blocks, ctypes.byref(n), s))
+        _check(fn(sink.data_ptr(), grid, blocks, ctypes.byref(n), s))
         b.record()
         b.synchronize()
         ms = a.elapsed_time(b)
         best = ms if best is None else min(best, ms)
-    return {"blocks_per_s": n.value / (best / 1e3), "GBps_equiv": n.value * 64 / (best / 1e3) / 1e9, "ms": best,
-            "blocks": n.value}
+    return {"blocks_per_s": n.value / (best / 1e3), "GBps_equiv": n.value * block_bytes / (best / 1e3) / 1e9,
+            "ms": best, "blocks": n.value}
 
 
 def measure_hbm_read(nbytes=16 << 30, device="cuda", grid=None, reps=5) -> dict:
@@ -335,33 +403,36 @@ def leaf_kernel_ms() -> float:
 class Verifier:
     """Reusable workspaces for repeated hash -> per-message roots -> manifest -> verify."""
 
-    def __init__(self, device="cuda"):
+    def __init__(self, device="cuda", alg: str = "sha256"):
         self.device = torch.device(device)
+        self.alg, self.D = alg, _alg(alg)[1]
         self.ws_hash = Workspace(self.device)
         self.ws_tree = Workspace(self.device)
         self.ws_manifest = Workspace(self.device)
         self.ws_verify = Workspace(self.device)
 
     def leaf_digests(self, msgs, chunk_bytes: int):
-        return hv_hash_chunks(msgs, chunk_bytes, self.device, self.ws_hash)
+        return hv_hash_chunks(msgs, chunk_bytes, self.device, self.ws_hash, alg=self.alg)
 
     def roots(self, msgs, chunk_bytes: int):
-        """(per-message roots [n, 32], leaf digests, seg_offsets)."""
+        """(per-message roots [n, D], leaf digests, seg_offsets)."""
         leaves, seg = self.leaf_digests(msgs, chunk_bytes)
-        return hv_merkle_reduce(leaves, seg, self.ws_tree), leaves, seg
+        return hv_merkle_reduce(leaves, seg, self.ws_tree, alg=self.alg), leaves, seg
 
     def manifest_root(self, msgs, chunk_bytes: int) -> torch.Tensor:
-        """One root over the per-message roots, in message order ([1, 32] device)."""
+        """One root over the per-message roots, in message order ([1, D] device)."""
         roots, _, _ = self.roots(msgs, chunk_bytes)
-        return hv_merkle_reduce(roots, np.array([0, roots.shape[0]], dtype=np.uint64), self.ws_manifest)
+        return hv_merkle_reduce(roots, np.array([0, roots.shape[0]], dtype=np.uint64), self.ws_manifest,
+                                alg=self.alg)
 
     def single_tree_root(self, msgs, chunk_bytes: int) -> torch.Tensor:
-        """One root over all leaf digests of all messages ([1, 32] device)."""
+        """One root over all leaf digests of all messages ([1, D] device)."""
         leaves, _ = self.leaf_digests(msgs, chunk_bytes)
-        return hv_merkle_reduce(leaves, np.array([0, leaves.shape[0]], dtype=np.uint64), self.ws_tree)
+        return hv_merkle_reduce(leaves, np.array([0, leaves.shape[0]], dtype=np.uint64), self.ws_tree,
+                                alg=self.alg)
 
     def verify_root(self, root: torch.Tensor, expected: bytes) -> bool:
-        return hv_verify_root(root.reshape(-1)[:32], expected, self.ws_verify)
+        return hv_verify_root(root.reshape(-1)[:self.D], expected, self.ws_verify, alg=self.alg)
 
 
 class Pipeline:
@@ -373,9 +444,11 @@ class Pipeline:
     returns its verdict.  Outputs and workspaces are allocated here, once.
     """
 
-    def __init__(self, msgs, chunk_bytes: int, mode: str = "manifest", device="cuda"):
+    def __init__(self, msgs, chunk_bytes: int, mode: str = "manifest", device="cuda", alg: str = "sha256"):
         if mode not in ("manifest", "single"):
             raise ValueError(mode)
+        self.alg, self.D = alg, _alg(alg)[1]
+        D = self.D
         self.device = torch.device(device)
         self.mode, self.C = mode, int(chunk_bytes)
         ptrs, lens = _ptr_len(msgs)
@@ -384,40 +457,38 @@ class Pipeline:
         self.n_msgs = len(self.arr)
         self.seg, self.n_leaves = hv_leaf_layout(ptrs, lens, self.C)
         self.total_bytes = int(np.asarray(lens, dtype=np.uint64).sum()) if self.n_msgs else 0
-        self.leaves = torch.empty((self.n_leaves, 32), dtype=torch.uint8, device=self.device)
+        self.leaves = torch.empty((self.n_leaves, D), dtype=torch.uint8, device=self.device)
         self.ws_hash = Workspace(self.device).get(lib.hv_hash_workspace_bytes(self.n_msgs, self.n_leaves))
         if mode == "manifest":
             self.tree_seg = self.seg
-            self.roots = torch.empty((self.n_msgs, 32), dtype=torch.uint8, device=self.device)
+            self.roots = torch.empty((self.n_msgs, D), dtype=torch.uint8, device=self.device)
             self.top_seg = np.array([0, self.n_msgs], dtype=np.uint64)
-            self.ws_top = Workspace(self.device).get(lib.hv_merkle_workspace_bytes(self.n_msgs, 1))
+            self.ws_top = Workspace(self.device).get(_merkle_ws_bytes(alg, self.n_msgs, 1))
         else:
             self.tree_seg = np.array([0, self.n_leaves], dtype=np.uint64)
-            self.roots = torch.empty((1, 32), dtype=torch.uint8, device=self.device)
+            self.roots = torch.empty((1, D), dtype=torch.uint8, device=self.device)
         self.ws_tree = Workspace(self.device).get(
-            lib.hv_merkle_workspace_bytes(int(self.tree_seg[-1]), len(self.tree_seg) - 1))
-        self.root = torch.empty((1, 32), dtype=torch.uint8, device=self.device)
+            _merkle_ws_bytes(alg, int(self.tree_seg[-1]), len(self.tree_seg) - 1))
+        self.root = torch.empty((1, D), dtype=torch.uint8, device=self.device)
         self.ws_verify = Workspace(self.device).get(lib.hv_verify_workspace_bytes())
 
     def compute(self):
-        """Queue the digests and roots on the current stream; returns the [1, 32] root."""
+        """Queue the digests and roots on the current stream; returns the [1, D] root."""
         s = _stream(self.device)
-        _check(lib.hv_hash_chunks(self.arr.ctypes.data if self.n_msgs else None, self.n_msgs, self.C,
-                                  self.leaves.data_ptr() if self.n_leaves else None,
-                                  self.ws_hash.data_ptr(), self.ws_hash.numel(), s))
-        _check(lib.hv_merkle_reduce(self.leaves.data_ptr() if self.n_leaves else None, self.tree_seg.ctypes.data,
-                                    len(self.tree_seg) - 1, self.roots.data_ptr(),
-                                    self.ws_tree.data_ptr(), self.ws_tree.numel(), s))
+        _check(_hash_call(self.alg, self.arr.ctypes.data if self.n_msgs else None, self.n_msgs, self.C,
+                          self.leaves.data_ptr() if self.n_leaves else None, self.ws_hash, s))
+        _check(_merkle_call(self.alg, self.leaves.data_ptr() if self.n_leaves else None, self.tree_seg.ctypes.data,
+                            len(self.tree_seg) - 1, self.roots.data_ptr(), self.ws_tree, s))
         if self.mode == "single":
             return self.roots
-        _check(lib.hv_merkle_reduce(self.roots.data_ptr() if self.n_msgs else None, self.top_seg.ctypes.data, 1,
-                                    self.root.data_ptr(), self.ws_top.data_ptr(), self.ws_top.numel(), s))
+        _check(_merkle_call(self.alg, self.roots.data_ptr() if self.n_msgs else None, self.top_seg.ctypes.data, 1,
+                            self.root.data_ptr(), self.ws_top, s))
         return self.root
 
     def run(self, expected: bytes) -> bool:
         """The whole path: digests, roots, comparison with ``expected`` (synchronous)."""
         root = self.compute()
-        return hv_verify_root(root, expected, _FixedWorkspace(self.ws_verify))
+        return hv_verify_root(root, expected, _FixedWorkspace(self.ws_verify), alg=self.alg)
 
 
 class Tree:
@@ -481,20 +552,20 @@ class _FixedWorkspace:
         return self.buf
 
 
-def manifest_root(named_tensors, chunk_bytes: int) -> bytes:
+def manifest_root(named_tensors, chunk_bytes: int, alg: str = "sha256") -> bytes:
     """Manifest root of {name: tensor} (byte-wise name order) or [(name, tensor)] (given order)."""
     items = sorted(named_tensors.items(), key=lambda kv: kv[0].encode("utf-8")) \
         if isinstance(named_tensors, dict) else list(named_tensors)
     dev = items[0][1].device if items else torch.device("cuda")
-    root = Verifier(dev).manifest_root([t for _, t in items], chunk_bytes)
+    root = Verifier(dev, alg).manifest_root([t for _, t in items], chunk_bytes)
     return bytes(root.cpu().numpy().reshape(-1))
 
 
-def verify(named_tensors, expected: bytes, chunk_bytes: int) -> None:
+def verify(named_tensors, expected: bytes, chunk_bytes: int, alg: str = "sha256") -> None:
     """Raise VerificationError unless the manifest root of the tensors equals ``expected``."""
     items = sorted(named_tensors.items(), key=lambda kv: kv[0].encode("utf-8")) \
         if isinstance(named_tensors, dict) else list(named_tensors)
-    v = Verifier(items[0][1].device)
+    v = Verifier(items[0][1].device, alg)
     root = v.manifest_root([t for _, t in items], chunk_bytes)
     if not v.verify_root(root, expected):
         raise VerificationError("model root does not match the expected root")

@@ -179,3 +179,51 @@ def test_incremental_rejects_before_launch():
 def test_timing_query_without_timed_call():
     with pytest.raises(hv.HVError):
         hv.leaf_kernel_ms()
+
+
+def test_sha384_kernel_constants_match_their_definition():
+    # the SHA-384 tables of the HIP source, re-derived from primes (FIPS 180-4 4.2.3, 5.3.4)
+    from test_oracle_sha256 import first_primes, iroot
+
+    src = open(os.path.join(ROOT, "paper_2510_23938_amd", "csrc", "sha384_device.h")).read()
+    k_body = re.search(r"kRound512\[80\]\s*=\s*\{(.*?)\};", src, re.S).group(1)
+    h_body = re.search(r"kInit384\[8\]\s*=\s*\{(.*?)\};", src, re.S).group(1)
+    K = [int(x, 16) for x in re.findall(r"0x([0-9a-fA-F]+)ull", k_body)]
+    H = [int(x, 16) for x in re.findall(r"0x([0-9a-fA-F]+)ull", h_body)]
+    p = first_primes(80)
+    assert K == [iroot(q << 192, 3) & ((1 << 64) - 1) for q in p]
+    assert H == [iroot(q << 128, 2) & ((1 << 64) - 1) for q in p[8:16]]
+
+
+def test_alg_entry_points_reject_before_launch():
+    ptrs, lens = _msgs([1000, 64])
+    arr = hv._msg_array(ptrs, lens)
+    p = arr.ctypes.data
+    for bad in (2, -1):
+        assert hv.lib.hv_hash_chunks_alg(bad, p, 2, 64, 0x1000, 0x100000, 1 << 30, None) == hv.HV_ERR_INVALID_ARG
+        assert b"unknown algorithm" in hv.lib.hv_last_error()
+        assert hv.lib.hv_merkle_workspace_bytes_alg(bad, 100, 1) == 0
+        seg = np.array([0, 5], dtype=np.uint64)
+        assert hv.lib.hv_merkle_reduce_alg(bad, 0x1000, seg.ctypes.data, 1, 0x2000, 0x100000, 1 << 20, None) == \
+            hv.HV_ERR_INVALID_ARG
+        exp = (ctypes.c_uint8 * 48)()
+        m = ctypes.c_int(0)
+        assert hv.lib.hv_verify_root_alg(bad, 0x1000, exp, ctypes.byref(m), 0x1000, 256, None) == \
+            hv.HV_ERR_INVALID_ARG
+        assert hv.lib.hv_compare_roots_alg(bad, 0x1000, 0x2000, 1, 0x3000, None) == hv.HV_ERR_INVALID_ARG
+    # SHA-384 chunks must be whole 128-byte blocks
+    for C in (64, 192, 4096 + 64):
+        st = hv.lib.hv_hash_chunks_alg(hv.HV_SHA384, p, 2, C, 0x1000, 0x100000, 1 << 30, None)
+        assert st == hv.HV_ERR_INVALID_ARG and b"multiple of 128" in hv.lib.hv_last_error()
+    # the SHA-256 form of the same call takes C = 64 and fails only at its workspace check
+    assert hv.lib.hv_hash_chunks_alg(hv.HV_SHA256, p, 2, 64, 0x1000, 0x100000, 16, None) == hv.HV_ERR_WORKSPACE
+    # SHA-384 Merkle workspace covers 48-byte nodes
+    assert hv.lib.hv_merkle_workspace_bytes_alg(hv.HV_SHA384, 1 << 20, 3) > \
+        hv.lib.hv_merkle_workspace_bytes_alg(hv.HV_SHA256, 1 << 20, 3)
+    assert hv.lib.hv_merkle_workspace_bytes_alg(hv.HV_SHA256, 1 << 20, 3) == hv.lib.hv_merkle_workspace_bytes(1 << 20, 3)
+
+
+def test_binding_checks_root_sizes():
+    with pytest.raises(ValueError):
+        hv._alg("sha512")
+    assert hv.ALGS["sha384"][1] == 48 and hv.ALGS["sha256"][1] == 32

@@ -8,9 +8,10 @@ times, against the CPU oracle.
   per-tensor root and the manifest against the oracle's closed form (RFC 6962
   over constant chunks, memoised); with random bf16 weights, every leaf
   digest, per-tensor root and the manifest against the threaded oracle,
-  streamed tensor by tensor; then a seeded one-byte flip in the weights (the
-  manifest changes and the per-tensor comparison names exactly the flipped
-  tensor) and a flipped byte of the expected root (verification fails).
+  streamed tensor by tensor, with SHA-256 and again with SHA-384; then a
+  seeded one-byte flip in the weights (the manifest changes and the per-tensor
+  comparison names exactly the flipped tensor) and a flipped byte of the
+  expected root (verification fails).
 """
 import gc
 import hashlib
@@ -136,6 +137,28 @@ def test_70b_random_weights_full_oracle(w70b):
         roots.append(oracle.mth(want))
     assert [bytes(r) for r in pipe.roots.cpu().numpy()] == roots
     assert root == oracle.mth(roots)
+
+
+@pytest.mark.timeout(900)
+def test_70b_random_weights_sha384_full_oracle(w70b):
+    # the same 141 GB of weights through the SHA-384 path (48-byte digests
+    # and nodes), every leaf digest and root against the threaded oracle
+    wl, _, _ = w70b
+    C = wl.chunk_bytes
+    pipe = hv.Pipeline(wl.msgs, C, "manifest", DEV, alg="sha384")
+    root = bytes(pipe.compute().cpu().numpy().reshape(-1))
+    gpu_leaves = pipe.leaves.cpu().numpy()
+    roots = []
+    for m, view in enumerate(wl.msgs.views):
+        want = oracle.leaf_digests_mt([view.cpu().numpy()], C, threads(), "sha384")
+        lo, hi = int(pipe.seg[m]), int(pipe.seg[m + 1])
+        assert np.array_equal(gpu_leaves[lo:hi], want), f"tensor {wl.msgs.names[m]}: SHA-384 leaf digests differ"
+        roots.append(oracle.mth(want, "sha384"))
+    assert [bytes(r) for r in pipe.roots.cpu().numpy()] == roots
+    assert root == oracle.mth(roots, "sha384")
+    assert pipe.run(root)
+    del pipe
+    free()
 
 
 @pytest.mark.timeout(600)

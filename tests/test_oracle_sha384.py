@@ -67,3 +67,24 @@ def test_chunk_digests_are_plain_sha384_of_slices(C):
         want = [hashlib.sha384(m).digest()] if C == 0 else \
             [hashlib.sha384(m[i:i + C]).digest() for i in range(0, n, C)]
         assert got == want, (n, C)
+
+
+@pytest.mark.parametrize("nthreads", [1, 3, 8])
+def test_threaded_drivers_are_hashlib_per_chunk(nthreads):
+    # both threaded drivers (separate messages, and messages packed in one
+    # buffer at offsets) against hashlib over each chunk slice
+    rng = np.random.default_rng(33)
+    lens = [0, 1, 111, 112, 128, 300, 4096, 4097, 0, 9000]
+    offs, pos = [], 0
+    for n in lens:
+        offs.append(pos)
+        pos += (n + 63) // 64 * 64
+    buf = rng.integers(0, 256, max(pos, 1), dtype=np.uint8)
+    msgs = [buf[o:o + n].tobytes() for o, n in zip(offs, lens)]
+    for C in (128, 1024, 0):
+        want = [hashlib.sha384(m).digest() for m in msgs] if C == 0 else \
+            [hashlib.sha384(m[i:i + C]).digest() for m in msgs for i in range(0, len(m), C)]
+        got = oracle.leaf_digests_mt(msgs, C, nthreads, "sha384")
+        assert [bytes(r) for r in got] == want, C
+        got = oracle.leaf_digests_mt_packed(buf, offs, lens, C, nthreads, "sha384")
+        assert [bytes(r) for r in got] == want, C
