@@ -261,6 +261,159 @@ def incremental_bench(args, dev):
     }), flush=True)
 
 
+def monitor_bench(args, dev):
+    """Continuous runtime monitoring beside inference-shaped work on the same
+    weights: the slowdown of that work against the monitor's verification
+    rate, per slice length (the monitor's budget)."""
+    import torch
+    import torch.nn.functional as F
+    import workloads as W
+    from paper_2510_23938_amd import hv
+
+    wl = W.workload(5, dev)
+    C, alg = wl.chunk_bytes, args.alg
+    pipe = hv.Pipeline(wl.msgs, C, "manifest", dev, alg=alg)
+    expected = bytes(pipe.compute().cpu().numpy().reshape(-1))
+    assert pipe.run(expected)  # the initial verification; its leaf digests are the monitor's references
+    ref = pipe.leaves
+    named = dict(zip(wl.msgs.names, wl.msgs.owners))
+    proj = ("self_attn.q_proj", "self_attn.k_proj", "self_attn.v_proj", "self_attn.o_proj", "mlp.gate_proj",
+            "mlp.up_proj", "mlp.down_proj")
+    layers = [[named[f"model.layers.{l}.{p}.weight"] for p in proj] for l in range(80)]
+    # two streams, made once and reused: streams beyond the device's hardware
+    # queues share queues, and a monitor stream sharing the inference stream's
+    # queue would run after it instead of beside it
+    inf = torch.cuda.Stream(dev)
+    mon_stream = torch.cuda.Stream(dev)
+
+    def workload_of(tokens, mats):
+        with torch.cuda.stream(inf):
+            xs = {d: torch.randn(tokens, d, device=dev, dtype=torch.bfloat16) for d in {w.shape[1] for w in mats}}
+
+        def step():
+            for w in mats:
+                F.linear(xs[w.shape[1]], w)
+        return step, sum(w.numel() * 2 for w in mats), sum(2 * tokens * w.numel() for w in mats)
+
+    kinds = {
+        "decode": workload_of(args.decode_batch, [w for L in layers for w in L] + [named["lm_head.weight"]]),
+        "prefill": workload_of(2048, [w for L in layers[:8] for w in L]),
+    }
+
+    def timed(step, n):
+        with torch.cuda.stream(inf):
+            step()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(inf)
+            for _ in range(n):
+                step()
+            b.record(inf)
+        b.synchronize()
+        return a, b
+
+    seg = pipe.seg
+    lens = wl.msgs.lens.astype(np.int64)
+
+    def leaf_bytes(first, count):
+        # bytes of leaves [first, first + count): full chunks except each message's last
+        m0 = int(np.searchsorted(seg, first, side="right")) - 1
+        m1 = int(np.searchsorted(seg, first + count - 1, side="right")) - 1
+        total = 0
+        for m in range(m0, m1 + 1):
+            lo, hi = max(first, int(seg[m])), min(first + count, int(seg[m + 1]))
+            if hi <= lo:
+                continue
+            last = int(seg[m + 1]) - 1
+            total += (hi - lo) * C
+            if lo <= last < hi:
+                total -= C - (int(lens[m]) - (last - int(seg[m])) * C)
+        return total
+
+    def run_monitor(slice_leaves, seconds, ring):
+        """Queue about `seconds` of scans (at the solo rate) back to back; returns (monitor, t0 event, [(end event, bytes)])."""
+        mon = hv.Monitor(wl.msgs, C, ref, alg, slice_leaves, dev, stream=mon_stream, ring=ring)
+        t0 = torch.cuda.Event(enable_timing=True)
+        t0.record(mon.stream)
+        ends = []
+        for _ in range(ring - 1):
+            first, count = mon.step()
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(mon.stream)
+            ends.append((e, leaf_bytes(first, count)))
+        return mon, t0, ends
+
+    # each kind alone
+    alone = {}
+    for kind, (step, wbytes, flops) in kinds.items():
+        a, b = timed(step, args.steps)
+        alone[kind] = a.elapsed_time(b) / args.steps
+        log(f"{kind} alone: {alone[kind]:.2f} ms/step ({wbytes / alone[kind] / 1e6:.0f} GB/s of weights, "
+            f"{flops / alone[kind] / 1e9:.0f} TFLOP/s)")
+    rows = []
+    for S in args.monitor_slices:
+        # the monitor alone at this slice length
+        probe = max(8, min(400, int(2 ** 30 * 4 / (S * C)) + 8))
+        mon, t0, ends = run_monitor(S, 0, probe)
+        ends[-1][0].synchronize()
+        ms = t0.elapsed_time(ends[-1][0])
+        solo = sum(nb for _, nb in ends) / (ms / 1e3) / 1e9
+        mon.poll(wait=True)
+        assert mon.mismatches == []
+        row = {"slice_leaves": S, "slice_bytes": S * C, "monitor_alone_GBps": round(solo, 1)}
+        for kind, (step, wbytes, flops) in kinds.items():
+            window = args.steps * alone[kind] / 1e3
+            n_scans = int(2.0 * window * solo * 1e9 / (S * C)) + 8
+            mon, t0, ends = run_monitor(S, window, n_scans + 1)
+            a, b = timed(step, args.steps)
+            ends[-1][0].synchronize()
+            ta, tb = t0.elapsed_time(a), t0.elapsed_time(b)
+            inside = [nb for e, nb in ends if ta < t0.elapsed_time(e) <= tb]
+            last_end = t0.elapsed_time(ends[-1][0])
+            co = a.elapsed_time(b) / args.steps
+            rate = sum(inside) / ((tb - ta) / 1e3) / 1e9
+            mon.poll(wait=True)
+            assert mon.mismatches == [], "the monitor reported a change in untouched weights"
+            slow = (co / alone[kind] - 1) * 100
+            sweep = pipe.total_bytes / (rate * 1e9) if rate > 0 else None
+            row[kind] = {"alone_ms": round(alone[kind], 3), "with_monitor_ms": round(co, 3),
+                         "slowdown_pct": round(slow, 2), "monitor_GBps": round(rate, 1),
+                         "monitor_busy_whole_window": last_end > tb,
+                         "sweep_s": round(sweep, 3) if sweep else None,
+                         # one sweep per interval, at this slice length: the average cost over the interval
+                         f"avg_slowdown_pct_at_{args.monitor_interval:g}s_interval":
+                             round(slow * min(1.0, sweep / args.monitor_interval), 3) if sweep else None}
+            log(f"slice {S}: {kind} {alone[kind]:.2f} -> {co:.2f} ms/step ({slow:+.1f}%), monitor {rate:.0f} GB/s "
+                f"(alone {solo:.0f}), sweep {row[kind]['sweep_s']} s")
+        rows.append(row)
+    # a changed byte is found, at its leaf, by one sweep
+    rng = np.random.default_rng(W.seed_of(5) + 11)
+    m = int(rng.integers(0, len(wl.msgs)))
+    off = int(rng.integers(0, int(lens[m])))
+    view = wl.msgs.views[m]
+    old = int(view[off].item())
+    view[off] = old ^ 0x80
+    torch.cuda.synchronize()
+    mon = hv.Monitor(wl.msgs, C, ref, alg, 16384, dev, stream=mon_stream, ring=256)
+    mon.sweep()
+    mon.poll(wait=True)
+    view[off] = old
+    torch.cuda.synchronize()
+    detected = [(fb, cnt) for fb, cnt, _, _ in mon.mismatches] == [(int(seg[m]) + off // C, 1)]
+    pick = min(rows, key=lambda r: abs(r["slice_leaves"] - args.monitor_slice))
+    line = {
+        "metric": "decode slowdown (%) with continuous monitoring of the resident weights beside it, 1 MI355X",
+        "value": pick["decode"]["slowdown_pct"], "unit": "%", "n_gpus": 1, "steps": args.steps, "warmup": 1,
+        "ms_per_step": pick["decode"]["with_monitor_ms"], "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+        "config": {"workload": "70B-shaped bf16 weight set (723 tensors, 64 KiB chunks) monitored while "
+                               f"decode-shaped (batch {args.decode_batch}, all 560 projections + lm_head) or "
+                               "prefill-shaped (2048 tokens, 8 layers) bf16 GEMMs run on the same weights",
+                   "hash": alg, "monitor_slice_leaves": pick["slice_leaves"], "monitor_duty": "100% (back to back)",
+                   "changed_byte_detected_at_its_leaf": detected, "slices": rows},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -279,6 +432,14 @@ def main():
     ap.add_argument("--incremental", type=int, default=0, metavar="K",
                     help="instead: change K random chunks of the workload and time re-verification that rehashes "
                          "only them and updates only their tree branches, against a full re-verification")
+    ap.add_argument("--monitor", action="store_true",
+                    help="instead: continuous monitoring of the 70B-shaped set beside decode- and prefill-shaped "
+                         "GEMMs on the same weights; slowdown vs monitor rate per slice length")
+    ap.add_argument("--monitor-slices", type=int, nargs="+", default=[1024, 4096, 16384, 65536])
+    ap.add_argument("--monitor-slice", type=int, default=4096, help="slice length of the reported value")
+    ap.add_argument("--decode-batch", type=int, default=8)
+    ap.add_argument("--monitor-interval", type=float, default=30.0,
+                    help="seconds between sweeps for the averaged cost (the paper's runtime-monitoring example)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 4 GiB device copy first (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -299,6 +460,9 @@ def main():
         return
     if args.incremental > 0:
         incremental_bench(args, dev)
+        return
+    if args.monitor:
+        monitor_bench(args, dev)
         return
     if args.copy_calibration:
         a = torch.empty(4 << 30, dtype=torch.uint8, device=dev)

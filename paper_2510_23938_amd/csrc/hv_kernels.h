@@ -54,6 +54,15 @@ hipError_t launch_sched_select(const MsgDesc* msgs, const Pair* off, uint32_t n,
 
 // SHA-256 of the n_slots leaves of a leaf table (sha256_leaves.hip); digests
 // go to digests + 32 * desc.out for desc.out < out_bound.
+// Leaf table of leaves [first, first + k) into desc[0..k) (digest slot e for
+// leaf first + e); also resets reset[0] = 0, reset[1] = ~0 when reset != NULL.
+hipError_t launch_sched_range(const MsgDesc* msgs, const Pair* off, uint32_t n, uint64_t C, uint64_t first,
+                              uint64_t k, LeafDesc* desc, uint64_t* reset, hipStream_t s);
+// Monitor comparison: for e < k, digest e (D bytes at digests + D*e) against
+// reference leaf first + e (ref + D*(first + e)); result[0] += mismatches,
+// result[1] = min(result[1], lowest mismatching leaf number).  D is 32 or 48.
+hipError_t launch_monitor_compare(const uint8_t* digests, const uint8_t* ref, uint64_t first, uint64_t k, uint32_t D,
+                                  uint64_t* result, hipStream_t s);
 hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                                 hipStream_t s);
 

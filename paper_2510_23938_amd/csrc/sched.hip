@@ -224,6 +224,36 @@ __global__ void __launch_bounds__(kThreads) select_kernel(const MsgDesc* __restr
     }
 }
 
+// Leaf table of a contiguous range of leaf numbers [first, first + k), slot e
+// writing digest e; block 0's first lane also resets a monitor result pair
+// (mismatch count 0, lowest mismatching leaf ~0), so that the comparison that
+// follows on the same stream starts from a clean result.
+__global__ void __launch_bounds__(kThreads) range_select_kernel(const MsgDesc* __restrict__ msgs,
+                                                                const Pair* __restrict__ off, uint32_t n, uint64_t C,
+                                                                uint64_t first, uint64_t k, LeafDesc* __restrict__ desc,
+                                                                uint64_t* __restrict__ reset) {
+    if (reset != nullptr && blockIdx.x == 0 && threadIdx.x == 0) {
+        reset[0] = 0;
+        reset[1] = ~0ull;
+    }
+    for (uint64_t e = (uint64_t)blockIdx.x * kThreads + threadIdx.x; e < k; e += (uint64_t)gridDim.x * kThreads) {
+        const uint64_t leaf = first + e;
+        const uint32_t m = find_leaf_owner(off, n, leaf);
+        const MsgDesc msg = msgs[m];
+        const uint64_t i = leaf - (off[m].x + off[m].y);
+        LeafDesc d;
+        if (C == 0) {
+            d.src = msg.data;
+            d.nbytes = msg.nbytes;
+        } else {
+            d.src = msg.data + i * C;
+            d.nbytes = msg.nbytes - i * C < C ? msg.nbytes - i * C : C;
+        }
+        d.out = e;
+        desc[e] = d;
+    }
+}
+
 unsigned grid_for(uint64_t n) {
     const uint64_t blocks = (n + kThreads - 1) / kThreads;
     const uint64_t cap = 65536;  // grid-stride loops cover the rest
@@ -266,6 +296,12 @@ hipError_t launch_sched_select(const MsgDesc* msgs, const Pair* off, uint32_t n,
                                uint64_t k, LeafDesc* desc, hipStream_t s) {
     if (k == 0) return hipSuccess;
     select_kernel<<<grid_for(k), kThreads, 0, s>>>(msgs, off, n, C, leaves, k, desc);
+    return hipGetLastError();
+}
+
+hipError_t launch_sched_range(const MsgDesc* msgs, const Pair* off, uint32_t n, uint64_t C, uint64_t first,
+                              uint64_t k, LeafDesc* desc, uint64_t* reset, hipStream_t s) {
+    range_select_kernel<<<grid_for(k), kThreads, 0, s>>>(msgs, off, n, C, first, k, desc, reset);
     return hipGetLastError();
 }
 

@@ -51,6 +51,8 @@ EXPORTS = (
     "hv_stream_workspace_bytes", "hv_hash_host_chunks",  # include/hv_stream.h
     "hv_tree_bytes", "hv_tree_build", "hv_tree_update_workspace_bytes", "hv_tree_update",
     "hv_rehash_workspace_bytes", "hv_rehash_chunks",  # include/hv_incremental.h
+    "hv_monitor_plan_bytes", "hv_monitor_init", "hv_monitor_scan_workspace_bytes",
+    "hv_monitor_scan",  # include/hv_monitor.h
 )
 
 
@@ -68,6 +70,11 @@ class VerificationError(Exception):
 
 class hv_msg(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("nbytes", ctypes.c_uint64)]
+
+
+class hv_monitor_plan(ctypes.Structure):
+    _fields_ = [("device", ctypes.c_void_p), ("alg", ctypes.c_int), ("n_msgs", ctypes.c_uint32),
+                ("chunk_bytes", ctypes.c_uint64), ("n_leaves", ctypes.c_uint64)]
 
 
 def _load():
@@ -106,6 +113,10 @@ def _load():
         "hv_tree_update": ([vp, vp, u32, vp, sz, vp, u32, vp, vp, sz, vp], ctypes.c_int),
         "hv_rehash_workspace_bytes": ([u32, u32], sz),
         "hv_rehash_chunks": ([vp, u32, u64, vp, u32, vp, vp, sz, vp], ctypes.c_int),
+        "hv_monitor_plan_bytes": ([u32], sz),
+        "hv_monitor_init": ([ctypes.c_int, vp, u32, u64, vp, sz, vp, vp], ctypes.c_int),
+        "hv_monitor_scan_workspace_bytes": ([ctypes.c_int, u64], sz),
+        "hv_monitor_scan": ([vp, u64, u64, vp, vp, vp, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -541,6 +552,105 @@ def leaves_of_range(seg_offsets, chunk_bytes: int, msg: int, lo: int, hi: int) -
     if chunk_bytes == 0:
         return np.array([first], dtype=np.uint64)
     return np.arange(first + lo // chunk_bytes, first + (hi - 1) // chunk_bytes + 1, dtype=np.uint64)
+
+
+class Monitor:
+    """Continuous runtime monitoring of resident weights (include/hv_monitor.h).
+
+    ``ref_digests`` are the leaf digests recorded when the weights were
+    verified against their expected root ([n_leaves, D] device tensor, leaf
+    order of ``hv_leaf_layout``).  Each ``scan`` rehashes ``slice_leaves``
+    consecutive leaves on the monitor's own stream and compares them with
+    their references; consecutive scans sweep the whole set round-robin.
+    Each scan's result (mismatch count, lowest mismatching leaf) is copied on
+    the monitor stream into a pinned host ring of ``ring`` slots, which
+    ``poll`` reads once the scan's event has completed -- the monitor never
+    waits on, or makes the host wait for, the work of other streams.
+    """
+
+    def __init__(self, msgs, chunk_bytes: int, ref_digests: torch.Tensor, alg: str = "sha256",
+                 slice_leaves: int = 4096, device="cuda", stream=None, ring: int = 64):
+        code, D = _alg(alg)
+        self.device = torch.device(device)
+        self.alg, self.D = alg, D
+        ptrs, lens = _ptr_len(msgs)
+        self.keepalive = msgs
+        arr = _msg_array(ptrs, lens)
+        n = len(arr)
+        self.plan = hv_monitor_plan()
+        self.plan_mem = Workspace(self.device).get(lib.hv_monitor_plan_bytes(n))
+        self.stream = stream or torch.cuda.Stream(self.device)
+        _check(lib.hv_monitor_init(code, arr.ctypes.data if n else None, n, chunk_bytes, self.plan_mem.data_ptr(),
+                                   self.plan_mem.numel(), ctypes.byref(self.plan), self.stream.cuda_stream))
+        self.n_leaves = int(self.plan.n_leaves)
+        if tuple(ref_digests.shape) != (self.n_leaves, D):
+            raise ValueError(f"ref_digests must be [{self.n_leaves}, {D}]")
+        self.ref = ref_digests
+        self.slice = max(1, min(int(slice_leaves), max(self.n_leaves, 1)))
+        self.ws = Workspace(self.device).get(lib.hv_monitor_scan_workspace_bytes(code, self.slice))
+        self.results = torch.empty((ring, 2), dtype=torch.int64, device=self.device)
+        self.host = torch.empty((ring, 2), dtype=torch.int64, pin_memory=True)
+        self.events = [None] * ring
+        self.ranges = [None] * ring
+        self.next_leaf = 0
+        self.issued = 0
+        self.read = 0
+        self.mismatches = []  # (first bad leaf, count, slice first, slice length) of each failing scan
+        self.stream.wait_stream(torch.cuda.current_stream(self.device))  # ref_digests were made there
+        self.stream.synchronize()  # the plan's upload and offsets are ready
+
+    def scan(self, first: int, count: int, slice_digests: torch.Tensor | None = None) -> torch.Tensor:
+        """Queue one scan of leaves [first, first + count) on the monitor stream; returns its result slot."""
+        ring = len(self.events)
+        slot = self.issued % ring
+        while self.read <= self.issued - ring:  # the slot's previous result is still unread
+            self.poll(wait=True, limit=1)
+        res = self.results[slot]
+        ws = self.ws if count <= self.slice else Workspace(self.device).get(
+            lib.hv_monitor_scan_workspace_bytes(_alg(self.alg)[0], count))
+        _check(lib.hv_monitor_scan(ctypes.byref(self.plan), first, count, self.ref.data_ptr(),
+                                   slice_digests.data_ptr() if slice_digests is not None else None,
+                                   res.data_ptr(), ws.data_ptr(), ws.numel(), self.stream.cuda_stream))
+        with torch.cuda.stream(self.stream):
+            self.host[slot].copy_(res, non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record(self.stream)
+        self.events[slot] = ev
+        self.ranges[slot] = (first, count)
+        self.issued += 1
+        return res
+
+    def step(self) -> tuple:
+        """Queue the next slice of the round-robin sweep; returns (first, count)."""
+        first = self.next_leaf
+        count = min(self.slice, self.n_leaves - first)
+        self.scan(first, count)
+        self.next_leaf = 0 if first + count >= self.n_leaves else first + count
+        return first, count
+
+    def sweep(self):
+        """Queue scans covering every leaf once, from leaf 0."""
+        self.next_leaf = 0
+        for _ in range(-(-self.n_leaves // self.slice)):
+            self.step()
+
+    def poll(self, wait: bool = False, limit: int | None = None) -> int:
+        """Read the results of completed scans, in issue order (waiting for
+        each with wait=True), at most ``limit`` of them; returns how many were read."""
+        done = 0
+        while self.read < self.issued and (limit is None or done < limit):
+            slot = self.read % len(self.events)
+            ev = self.events[slot]
+            if wait:
+                ev.synchronize()
+            elif not ev.query():
+                break
+            cnt, first_bad = (int(v) for v in self.host[slot].tolist())
+            if cnt:
+                self.mismatches.append((first_bad & 0xFFFFFFFFFFFFFFFF, cnt) + self.ranges[slot])
+            self.read += 1
+            done += 1
+        return done
 
 
 class _FixedWorkspace:

@@ -227,3 +227,39 @@ def test_binding_checks_root_sizes():
     with pytest.raises(ValueError):
         hv._alg("sha512")
     assert hv.ALGS["sha384"][1] == 48 and hv.ALGS["sha256"][1] == 32
+
+
+def test_monitor_rejects_before_launch():
+    ptrs, lens = _msgs([1000, 64])
+    arr = hv._msg_array(ptrs, lens)
+    p = arr.ctypes.data
+    plan = hv.hv_monitor_plan()
+    need = hv.lib.hv_monitor_plan_bytes(2)
+    assert need >= 2 * 16 and need % 256 == 0
+    assert hv.lib.hv_monitor_init(5, p, 2, 64, 0x100000, need, ctypes.byref(plan), None) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_monitor_init(0, p, 2, 64, 0x100000, need, None, None) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_monitor_init(0, p, 2, 100, 0x100000, need, ctypes.byref(plan), None) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_monitor_init(1, p, 2, 64, 0x100000, need, ctypes.byref(plan), None) == hv.HV_ERR_INVALID_ARG
+    assert b"multiple of 128" in hv.lib.hv_last_error()
+    assert hv.lib.hv_monitor_init(0, p, 2, 64, 0x100000, need - 1, ctypes.byref(plan), None) == hv.HV_ERR_WORKSPACE
+    assert hv.lib.hv_monitor_init(0, p, 2, 64, 0x100010, need, ctypes.byref(plan), None) == hv.HV_ERR_WORKSPACE
+    # scans of a plan filled by hand (never dereferenced: every case fails validation)
+    plan = hv.hv_monitor_plan(0x100000, 0, 2, 64, 17)
+    ws = hv.lib.hv_monitor_scan_workspace_bytes(0, 17)
+    assert ws >= 17 * (24 + 32) and hv.lib.hv_monitor_scan_workspace_bytes(1, 17) > ws
+    scan = lambda pl, first, n, ref=0x200000, out=None, res=0x300000, w=0x400000, wb=ws: \
+        hv.lib.hv_monitor_scan(pl, first, n, ref, out, res, w, wb, None)
+    assert scan(None, 0, 1) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(hv.hv_monitor_plan(None, 0, 2, 64, 17)), 0, 1) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(hv.hv_monitor_plan(0x100000, 7, 2, 64, 17)), 0, 1) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(plan), 10, 8) == hv.HV_ERR_INVALID_ARG and b"not within" in hv.lib.hv_last_error()
+    assert scan(ctypes.byref(plan), 18, 0) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(plan), 1, 2 ** 64 - 1) == hv.HV_ERR_INVALID_ARG   # no wrap-around
+    assert scan(ctypes.byref(plan), 0, 1, res=None) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(plan), 0, 1, res=0x300004) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(plan), 0, 1, ref=None) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(plan), 0, 1, ref=0x200008) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(plan), 0, 1, out=0x500004) == hv.HV_ERR_INVALID_ARG
+    assert scan(ctypes.byref(plan), 0, 17, wb=ws - 1) == hv.HV_ERR_WORKSPACE
+    assert scan(ctypes.byref(plan), 0, 17, w=0x400040) == hv.HV_ERR_WORKSPACE
+    assert scan(ctypes.byref(plan), 0, 17, w=None) == hv.HV_ERR_WORKSPACE
