@@ -440,6 +440,8 @@ def main():
     ap.add_argument("--decode-batch", type=int, default=8)
     ap.add_argument("--monitor-interval", type=float, default=30.0,
                     help="seconds between sweeps for the averaged cost (the paper's runtime-monitoring example)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time HIP-graph replays of the prepared pass (kernel timing from the eager passes)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 4 GiB device copy first (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -495,6 +497,19 @@ def main():
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     hv.set_kernel_timing(False)
+    eager_ms = dt / args.steps * 1e3
+    if args.graph:
+        # the same checked pass captured once in a HIP graph, then replayed
+        pipe.capture(expected)
+        for _ in range(args.warmup):
+            assert pipe.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            assert pipe.replay()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        log(f"graph replay: {dt / args.steps * 1e3:.2f} ms/step (eager {eager_ms:.2f})")
     # a flipped expected byte must fail, a matching one pass
     bad = bytearray(expected)
     bad[int(np.random.default_rng(W.seed_of(args.config) + 1).integers(0, len(bad)))] ^= 0x01
@@ -517,6 +532,8 @@ def main():
             "workload": wl.description, "config_index": args.config, "bytes": total, "messages": len(wl.msgs),
             "leaves": pipe.n_leaves, "chunk_bytes": wl.chunk_bytes, "hash": alg, f"{alg}_blocks": blocks,
             "verified": True, "mismatch_detected": negative_ok,
+            "step": "HIP graph replay of the prepared pass" if args.graph else "prepared pass, eager launches",
+            "eager_ms_per_step": round(eager_ms, 3),
         },
         "roofline": {
             "kernel": leaf_kernel, "bound": "alu", "achieved": round(achieved, 3), "peak": round(VALU_PEAK_TOPS, 3),

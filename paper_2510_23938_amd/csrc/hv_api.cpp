@@ -90,10 +90,7 @@ struct Timing {
 };
 thread_local Timing g_timing;
 
-// Merkle plan: O[0] = segment offsets, O[k][s] = first output node of segment
-// s after launch k (each segment gets max(1, ceil(count / 512)) tiles).  The
-// last row is 0, 1, ..., n_seg: one node (the root) per segment.
-constexpr int kMaxLaunches = 8;  // ceil(64 / 9): a 64-bit leaf count needs at most 8
+constexpr int kMaxLaunches = kMaxMerkleLaunches;
 
 struct MerkleLayout {
     uint64_t* table;
@@ -102,17 +99,13 @@ struct MerkleLayout {
     size_t bytes;
 };
 
-uint64_t tiles_bound(uint64_t n_nodes, uint32_t n_seg) {
-    return n_nodes / hv::kTileNodes + (uint64_t)n_seg + 1;
-}
-
 uint32_t digest_bytes(hv_alg alg) { return alg == HV_SHA384 ? 48 : 32; }
 
 MerkleLayout merkle_layout(void* ws, uint64_t n_nodes, uint32_t n_seg, uint32_t D) {
     Carver c(ws);
     MerkleLayout L;
     L.table = c.take<uint64_t>((size_t)(kMaxLaunches + 1) * ((size_t)n_seg + 1));
-    const uint64_t nb = tiles_bound(n_nodes, n_seg);
+    const uint64_t nb = merkle_tiles_bound(n_nodes, n_seg);
     L.ping = c.take<uint8_t>(nb * D);
     L.pong = c.take<uint8_t>(nb * D);
     L.bytes = c.used;
@@ -122,6 +115,34 @@ MerkleLayout merkle_layout(void* ws, uint64_t n_nodes, uint32_t n_seg, uint32_t 
 }  // namespace
 
 namespace hvh {
+
+uint64_t merkle_tiles_bound(uint64_t n_nodes, uint32_t n_seg) {
+    return n_nodes / hv::kTileNodes + (uint64_t)n_seg + 1;
+}
+
+hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches) {
+    const size_t row = (size_t)n_seg + 1;
+    table->assign(seg_offsets, seg_offsets + row);
+    int k = 0;
+    for (;;) {
+        std::vector<uint64_t> next(row);
+        next[0] = 0;
+        bool more = false;
+        for (uint32_t s = 0; s < n_seg; ++s) {
+            const uint64_t* prev = table->data() + (size_t)k * row;
+            const uint64_t c = prev[s + 1] - prev[s];
+            const uint64_t tiles = c <= (uint64_t)hv::kTileNodes ? 1 : (c + hv::kTileNodes - 1) / hv::kTileNodes;
+            if (tiles > 1) more = true;
+            next[s + 1] = next[s] + tiles;
+        }
+        table->insert(table->end(), next.begin(), next.end());
+        ++k;
+        if (!more) break;
+        if (k == kMaxMerkleLaunches) return fail(HV_ERR_INVALID_ARG, "tree too deep");
+    }
+    *launches = k;
+    return HV_OK;
+}
 
 // Scheduling kernels over device-resident descriptors: the leaf table of
 // n_msgs messages goes to L.desc (which must be sized for n_leaves).
@@ -203,21 +224,11 @@ hv_status hv_hash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, ui
                             &n_leaves);
     if (st != HV_OK || n_leaves == 0) return st;
 
-    hipError_t e;
-    Timing& T = g_timing;
-    if (T.enabled) {
-        if (!T.start && (e = hipEventCreate(&T.start)) != hipSuccess) return hip_fail(e, "event create");
-        if (!T.stop && (e = hipEventCreate(&T.stop)) != hipSuccess) return hip_fail(e, "event create");
-        if ((e = hipEventRecord(T.start, stream)) != hipSuccess) return hip_fail(e, "event record");
-    }
-    e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream)
-                         : hv::launch_sha256_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream);
+    if ((st = leaf_timing_start(stream)) != HV_OK) return st;
+    const hipError_t e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream)
+                                          : hv::launch_sha256_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream);
     if (e != hipSuccess) return hip_fail(e, "leaf kernel");
-    if (T.enabled) {
-        if ((e = hipEventRecord(T.stop, stream)) != hipSuccess) return hip_fail(e, "event record");
-        T.have = true;
-    }
-    return HV_OK;
+    return leaf_timing_stop(stream);
 }
 
 hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint8_t* leaf_digests,
@@ -277,24 +288,10 @@ hv_status hv_merkle_reduce_alg(hv_alg alg, const uint8_t* nodes, const uint64_t*
 
     // Plan on the host: rows of n_seg + 1 offsets, one per launch level.
     const size_t row = (size_t)n_seg + 1;
-    std::vector<uint64_t> table(seg_offsets, seg_offsets + row);
+    std::vector<uint64_t> table;
     int launches = 0;
-    for (;;) {
-        const uint64_t* prev = &table[(size_t)launches * row];
-        std::vector<uint64_t> next(row);
-        next[0] = 0;
-        bool more = false;
-        for (uint32_t s = 0; s < n_seg; ++s) {
-            const uint64_t c = prev[s + 1] - prev[s];
-            const uint64_t tiles = c <= (uint64_t)hv::kTileNodes ? 1 : (c + hv::kTileNodes - 1) / hv::kTileNodes;
-            if (tiles > 1) more = true;
-            next[s + 1] = next[s] + tiles;
-        }
-        table.insert(table.end(), next.begin(), next.end());
-        ++launches;
-        if (!more) break;
-        if (launches == kMaxLaunches) return fail(HV_ERR_INVALID_ARG, "tree too deep");
-    }
+    const hv_status st = merkle_plan(seg_offsets, n_seg, &table, &launches);
+    if (st != HV_OK) return st;
 
     const MerkleLayout L = merkle_layout(workspace, n_nodes, n_seg, D);
     hipError_t e = hipMemcpyAsync(L.table, table.data(), table.size() * sizeof(uint64_t), hipMemcpyHostToDevice,
@@ -358,6 +355,33 @@ hv_status hv_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32
                            hipStream_t stream) {
     return hv_compare_roots_alg(HV_SHA256, roots, expected, n, mismatch, stream);
 }
+
+}  // extern "C"
+
+namespace hvh {
+
+hv_status leaf_timing_start(hipStream_t stream) {
+    Timing& T = g_timing;
+    if (!T.enabled) return HV_OK;
+    hipError_t e;
+    if (!T.start && (e = hipEventCreate(&T.start)) != hipSuccess) return hip_fail(e, "event create");
+    if (!T.stop && (e = hipEventCreate(&T.stop)) != hipSuccess) return hip_fail(e, "event create");
+    if ((e = hipEventRecord(T.start, stream)) != hipSuccess) return hip_fail(e, "event record");
+    return HV_OK;
+}
+
+hv_status leaf_timing_stop(hipStream_t stream) {
+    Timing& T = g_timing;
+    if (!T.enabled) return HV_OK;
+    const hipError_t e = hipEventRecord(T.stop, stream);
+    if (e != hipSuccess) return hip_fail(e, "event record");
+    T.have = true;
+    return HV_OK;
+}
+
+}  // namespace hvh
+
+extern "C" {
 
 hv_status hv_set_kernel_timing(int enable) {
     g_timing.enabled = enable != 0;

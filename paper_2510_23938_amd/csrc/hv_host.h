@@ -4,6 +4,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "hv.h"
 #include "hv_kernels.h"
 
@@ -54,5 +56,23 @@ hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_
 // Scheduling kernels over device-resident descriptors into L (leaf table in L.desc).
 hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t n_full,
                          uint64_t n_leaves, const HashLayout& L, hipStream_t stream);
+
+// Segmented Merkle reductions chain launches of 9 levels each (512-node tiles).
+// A 64-bit node count needs at most ceil(64 / 9) = 8 launches.
+constexpr int kMaxMerkleLaunches = 8;
+
+// Host plan of a segmented Merkle reduction over validated segment offsets:
+// `table` gets rows of n_seg + 1 offsets -- row 0 the segment offsets, row k
+// the first output node of each segment after launch k (a segment with c
+// nodes gets max(1, ceil(c / 512)) tiles) -- and `launches` the launch count.
+hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches);
+
+// Nodes any launch of a reduction of n_nodes nodes in n_seg segments writes, at most.
+uint64_t merkle_tiles_bound(uint64_t n_nodes, uint32_t n_seg);
+
+// HIP events around a leaf kernel on `stream` when hv_set_kernel_timing is on
+// for this thread (no-ops otherwise).
+hv_status leaf_timing_start(hipStream_t stream);
+hv_status leaf_timing_stop(hipStream_t stream);
 
 }  // namespace hvh

@@ -93,6 +93,9 @@ hipError_t launch_tree_roots(const uint8_t* top, const uint64_t* top_off, uint32
 // nbytes: 32 or 48 (the digest size of the call's hash).
 hipError_t launch_verify_root(const uint8_t* root, const uint8_t* expected, uint32_t nbytes, uint32_t* flag,
                               hipStream_t s);
+// As launch_verify_root with `expected` (nbytes) in device memory.
+hipError_t launch_verify_root_dev(const uint8_t* root, const uint8_t* expected, uint32_t nbytes, uint32_t* flag,
+                                  hipStream_t s);
 hipError_t launch_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32_t n, uint32_t nbytes,
                                 uint32_t* mismatch, hipStream_t s);
 

@@ -24,6 +24,16 @@ __global__ void verify_root_kernel(const uint8_t* __restrict__ root, Expected e,
     *flag = diff == 0 ? 1u : 0u;
 }
 
+// The same comparison with the expected bytes in device memory, so that a
+// captured graph can check against whatever the caller last stored there.
+__global__ void verify_root_dev_kernel(const uint8_t* __restrict__ root, const uint8_t* __restrict__ expected,
+                                       uint32_t nwords, uint32_t* __restrict__ flag) {
+    if (blockIdx.x != 0 || threadIdx.x != 0) return;
+    uint32_t diff = 0;
+    for (uint32_t i = 0; i < nwords; ++i) diff |= load_le_word(root + 4 * i) ^ load_le_word(expected + 4 * i);
+    *flag = diff == 0 ? 1u : 0u;
+}
+
 __global__ void __launch_bounds__(256) compare_roots_kernel(const uint8_t* __restrict__ roots,
                                                             const uint8_t* __restrict__ expected, uint32_t n,
                                                             uint32_t nbytes, uint32_t* __restrict__ mismatch) {
@@ -42,6 +52,12 @@ hipError_t launch_verify_root(const uint8_t* root, const uint8_t* expected, uint
     Expected e = {};
     for (uint32_t i = 0; i < nbytes && i < sizeof e.w; ++i) reinterpret_cast<uint8_t*>(e.w)[i] = expected[i];
     verify_root_kernel<<<1, 64, 0, s>>>(root, e, nbytes / 4, flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_verify_root_dev(const uint8_t* root, const uint8_t* expected, uint32_t nbytes, uint32_t* flag,
+                                  hipStream_t s) {
+    verify_root_dev_kernel<<<1, 64, 0, s>>>(root, expected, nbytes / 4, flag);
     return hipGetLastError();
 }
 

@@ -53,6 +53,7 @@ EXPORTS = (
     "hv_rehash_workspace_bytes", "hv_rehash_chunks",  # include/hv_incremental.h
     "hv_monitor_plan_bytes", "hv_monitor_init", "hv_monitor_scan_workspace_bytes",
     "hv_monitor_scan",  # include/hv_monitor.h
+    "hv_plan_bytes", "hv_plan_init", "hv_plan_run",  # include/hv_plan.h
 )
 
 
@@ -70,6 +71,16 @@ class VerificationError(Exception):
 
 class hv_msg(ctypes.Structure):
     _fields_ = [("data", ctypes.c_void_p), ("nbytes", ctypes.c_uint64)]
+
+
+HV_PLAN_MAX_LAUNCHES = 8
+
+
+class hv_verify_plan(ctypes.Structure):
+    _fields_ = [("device", ctypes.c_void_p), ("bytes", ctypes.c_size_t), ("alg", ctypes.c_int),
+                ("manifest", ctypes.c_int), ("n_msgs", ctypes.c_uint32), ("n_seg", ctypes.c_uint32),
+                ("chunk_bytes", ctypes.c_uint64), ("n_leaves", ctypes.c_uint64),
+                ("launches", ctypes.c_uint32 * 2), ("tiles", (ctypes.c_uint64 * HV_PLAN_MAX_LAUNCHES) * 2)]
 
 
 class hv_monitor_plan(ctypes.Structure):
@@ -113,6 +124,9 @@ def _load():
         "hv_tree_update": ([vp, vp, u32, vp, sz, vp, u32, vp, vp, sz, vp], ctypes.c_int),
         "hv_rehash_workspace_bytes": ([u32, u32], sz),
         "hv_rehash_chunks": ([vp, u32, u64, vp, u32, vp, vp, sz, vp], ctypes.c_int),
+        "hv_plan_bytes": ([ctypes.c_int, vp, u32, u64, ctypes.c_int], sz),
+        "hv_plan_init": ([ctypes.c_int, vp, u32, u64, ctypes.c_int, vp, sz, vp, vp], ctypes.c_int),
+        "hv_plan_run": ([vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
         "hv_monitor_plan_bytes": ([u32], sz),
         "hv_monitor_init": ([ctypes.c_int, vp, u32, u64, vp, sz, vp, vp], ctypes.c_int),
         "hv_monitor_scan_workspace_bytes": ([ctypes.c_int, u64], sz),
@@ -447,59 +461,95 @@ class Verifier:
 
 
 class Pipeline:
-    """One message set, marshalled once, run many times: the whole path.
+    """One message set, prepared once (include/hv_plan.h), run many times: the whole path.
 
     mode "manifest": chunk digests -> one root per message -> one root over
     those (hierarchical roots); mode "single": chunk digests -> one root over
     all of them.  ``run(expected)`` ends with the on-GPU root comparison and
-    returns its verdict.  Outputs and workspaces are allocated here, once.
+    returns its verdict.  The plan, outputs and the expected-root and verdict
+    buffers are allocated here, once; a pass only queues kernels, so
+    ``capture`` can record it in a HIP graph and ``replay`` re-runs it.
     """
 
     def __init__(self, msgs, chunk_bytes: int, mode: str = "manifest", device="cuda", alg: str = "sha256"):
         if mode not in ("manifest", "single"):
             raise ValueError(mode)
-        self.alg, self.D = alg, _alg(alg)[1]
-        D = self.D
+        code, D = _alg(alg)
+        self.alg, self.D = alg, D
         self.device = torch.device(device)
         self.mode, self.C = mode, int(chunk_bytes)
         ptrs, lens = _ptr_len(msgs)
         self.keepalive = msgs
-        self.arr = _msg_array(ptrs, lens)
-        self.n_msgs = len(self.arr)
+        arr = _msg_array(ptrs, lens)
+        self.n_msgs = len(arr)
         self.seg, self.n_leaves = hv_leaf_layout(ptrs, lens, self.C)
         self.total_bytes = int(np.asarray(lens, dtype=np.uint64).sum()) if self.n_msgs else 0
+        manifest = 1 if mode == "manifest" else 0
+        nbytes = lib.hv_plan_bytes(code, arr.ctypes.data if self.n_msgs else None, self.n_msgs, self.C, manifest)
+        if nbytes == 0:
+            raise HVError(HV_ERR_INVALID_ARG, lib.hv_last_error().decode("utf-8", "replace"))
+        self.plan_mem = Workspace(self.device).get(nbytes)
+        self.plan = hv_verify_plan()
+        _check(lib.hv_plan_init(code, arr.ctypes.data if self.n_msgs else None, self.n_msgs, self.C, manifest,
+                                self.plan_mem.data_ptr(), self.plan_mem.numel(), ctypes.byref(self.plan),
+                                _stream(self.device)))
         self.leaves = torch.empty((self.n_leaves, D), dtype=torch.uint8, device=self.device)
-        self.ws_hash = Workspace(self.device).get(lib.hv_hash_workspace_bytes(self.n_msgs, self.n_leaves))
-        if mode == "manifest":
-            self.tree_seg = self.seg
-            self.roots = torch.empty((self.n_msgs, D), dtype=torch.uint8, device=self.device)
-            self.top_seg = np.array([0, self.n_msgs], dtype=np.uint64)
-            self.ws_top = Workspace(self.device).get(_merkle_ws_bytes(alg, self.n_msgs, 1))
-        else:
-            self.tree_seg = np.array([0, self.n_leaves], dtype=np.uint64)
-            self.roots = torch.empty((1, D), dtype=torch.uint8, device=self.device)
-        self.ws_tree = Workspace(self.device).get(
-            _merkle_ws_bytes(alg, int(self.tree_seg[-1]), len(self.tree_seg) - 1))
-        self.root = torch.empty((1, D), dtype=torch.uint8, device=self.device)
-        self.ws_verify = Workspace(self.device).get(lib.hv_verify_workspace_bytes())
+        self.roots = torch.empty((max(int(self.plan.n_seg), 1), D), dtype=torch.uint8, device=self.device)
+        self.root = torch.empty((1, D), dtype=torch.uint8, device=self.device) if manifest else self.roots[:1]
+        self.expected_dev = torch.zeros(D, dtype=torch.uint8, device=self.device)
+        self.match_dev = torch.zeros(1, dtype=torch.int32, device=self.device)
+        self.match_host = torch.zeros(1, dtype=torch.int32, pin_memory=True)
+        self._expected = None
+        self.graph = None
+
+    def _run(self, check: bool, stream: int):
+        _check(lib.hv_plan_run(ctypes.byref(self.plan), self.leaves.data_ptr() if self.n_leaves else None,
+                               self.roots.data_ptr(), self.root.data_ptr(),
+                               self.expected_dev.data_ptr() if check else None,
+                               self.match_dev.data_ptr() if check else None, stream))
 
     def compute(self):
         """Queue the digests and roots on the current stream; returns the [1, D] root."""
-        s = _stream(self.device)
-        _check(_hash_call(self.alg, self.arr.ctypes.data if self.n_msgs else None, self.n_msgs, self.C,
-                          self.leaves.data_ptr() if self.n_leaves else None, self.ws_hash, s))
-        _check(_merkle_call(self.alg, self.leaves.data_ptr() if self.n_leaves else None, self.tree_seg.ctypes.data,
-                            len(self.tree_seg) - 1, self.roots.data_ptr(), self.ws_tree, s))
-        if self.mode == "single":
-            return self.roots
-        _check(_merkle_call(self.alg, self.roots.data_ptr() if self.n_msgs else None, self.top_seg.ctypes.data, 1,
-                            self.root.data_ptr(), self.ws_top, s))
+        self._run(False, _stream(self.device))
         return self.root
+
+    def set_expected(self, expected: bytes):
+        """Store the expected root on the device (only when it changed)."""
+        expected = bytes(expected)
+        if len(expected) != self.D:
+            raise ValueError(f"expected root must be {self.D} bytes for {self.alg}")
+        if expected != self._expected:
+            self.expected_dev.copy_(torch.frombuffer(bytearray(expected), dtype=torch.uint8))
+            self._expected = expected
+
+    def _verdict(self) -> bool:
+        s = torch.cuda.current_stream(self.device)
+        self.match_host.copy_(self.match_dev, non_blocking=True)
+        s.synchronize()
+        return int(self.match_host[0]) == 1
 
     def run(self, expected: bytes) -> bool:
         """The whole path: digests, roots, comparison with ``expected`` (synchronous)."""
-        root = self.compute()
-        return hv_verify_root(root, expected, _FixedWorkspace(self.ws_verify), alg=self.alg)
+        self.set_expected(expected)
+        self._run(True, _stream(self.device))
+        return self._verdict()
+
+    def capture(self, expected: bytes):
+        """Record one checked pass in a HIP graph (kernels only) for ``replay``."""
+        self.set_expected(expected)
+        torch.cuda.synchronize(self.device)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self._run(True, _stream(self.device))
+        self.graph = g
+        return g
+
+    def replay(self, expected: bytes | None = None) -> bool:
+        """Replay the captured pass (against ``expected`` if given, else the captured one); returns the verdict."""
+        if expected is not None:
+            self.set_expected(expected)
+        self.graph.replay()
+        return self._verdict()
 
 
 class Tree:
@@ -651,15 +701,6 @@ class Monitor:
             self.read += 1
             done += 1
         return done
-
-
-class _FixedWorkspace:
-    def __init__(self, buf):
-        self.buf = buf
-
-    def get(self, nbytes):
-        assert self.buf.numel() >= nbytes
-        return self.buf
 
 
 def manifest_root(named_tensors, chunk_bytes: int, alg: str = "sha256") -> bytes:

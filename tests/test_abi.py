@@ -263,3 +263,50 @@ def test_monitor_rejects_before_launch():
     assert scan(ctypes.byref(plan), 0, 17, wb=ws - 1) == hv.HV_ERR_WORKSPACE
     assert scan(ctypes.byref(plan), 0, 17, w=0x400040) == hv.HV_ERR_WORKSPACE
     assert scan(ctypes.byref(plan), 0, 17, w=None) == hv.HV_ERR_WORKSPACE
+
+
+def test_plan_rejects_before_launch():
+    ptrs, lens = _msgs([1000, 64, 0])
+    arr = hv._msg_array(ptrs, lens)
+    p = arr.ctypes.data
+    b = hv.lib.hv_plan_bytes(0, p, 3, 64, 1)
+    assert b > 0 and b % 256 == 0
+    assert hv.lib.hv_plan_bytes(1, p, 3, 128, 1) >= hv.lib.hv_plan_bytes(0, p, 3, 128, 1)  # 48-byte nodes
+    assert hv.lib.hv_plan_bytes(0, p, 3, 64, 0) > 0
+    assert hv.lib.hv_plan_bytes(0, None, 0, 64, 1) > 0                  # an empty set is a plan too
+    assert hv.lib.hv_plan_bytes(3, p, 3, 64, 1) == 0 and b"unknown algorithm" in hv.lib.hv_last_error()
+    assert hv.lib.hv_plan_bytes(0, p, 3, 100, 1) == 0
+    assert hv.lib.hv_plan_bytes(1, p, 3, 64, 1) == 0 and b"multiple of 128" in hv.lib.hv_last_error()
+    plan = hv.hv_verify_plan()
+    init = lambda *a: hv.lib.hv_plan_init(*a, None)
+    assert init(0, p, 3, 64, 1, 0x100000, b, None) == hv.HV_ERR_INVALID_ARG
+    assert init(0, p, 3, 64, 1, 0x100000, b - 1, ctypes.byref(plan)) == hv.HV_ERR_WORKSPACE
+    assert init(0, p, 3, 64, 1, 0x100080, b, ctypes.byref(plan)) == hv.HV_ERR_WORKSPACE
+    assert init(0, p, 3, 64, 1, None, b, ctypes.byref(plan)) == hv.HV_ERR_WORKSPACE
+    # runs of hand-filled plans that fail validation before any launch
+    good = dict(device=0x100000, bytes=1 << 20, alg=0, manifest=1, n_msgs=3, n_seg=3, chunk_bytes=64, n_leaves=17)
+    run = lambda pl, leaves=0x200000, roots=0x300000, root=0x400000, exp=None, match=None: \
+        hv.lib.hv_plan_run(ctypes.byref(pl) if pl is not None else None, leaves, roots, root, exp, match, None)
+
+    def mk(**kw):
+        d = dict(good)
+        d.update(kw)
+        pl = hv.hv_verify_plan()
+        for k, v in d.items():
+            setattr(pl, k, v)
+        pl.launches[0] = pl.launches[1] = 1
+        return pl
+    assert run(None) == hv.HV_ERR_INVALID_ARG
+    assert run(mk(device=None)) == hv.HV_ERR_INVALID_ARG
+    assert run(mk(alg=9)) == hv.HV_ERR_INVALID_ARG
+    bad = mk()
+    bad.launches[0] = 9
+    assert run(bad) == hv.HV_ERR_INVALID_ARG and b"corrupt" in hv.lib.hv_last_error()
+    assert run(mk(bytes=256)) == hv.HV_ERR_INVALID_ARG and b"corrupt" in hv.lib.hv_last_error()
+    assert run(mk(), leaves=None) == hv.HV_ERR_INVALID_ARG
+    assert run(mk(), roots=None) == hv.HV_ERR_INVALID_ARG
+    assert run(mk(), root=None) == hv.HV_ERR_INVALID_ARG
+    assert run(mk(), root=0x400008) == hv.HV_ERR_INVALID_ARG
+    assert run(mk(), exp=0x500000) == hv.HV_ERR_INVALID_ARG            # expected without match
+    assert run(mk(), match=0x600000) == hv.HV_ERR_INVALID_ARG          # match without expected
+    assert run(mk(), exp=0x500000, match=0x600002) == hv.HV_ERR_INVALID_ARG
