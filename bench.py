@@ -300,14 +300,15 @@ def monitor_bench(args, dev):
         "prefill": workload_of(2048, [w for L in layers[:8] for w in L]),
     }
 
-    def timed(step, n):
-        with torch.cuda.stream(inf):
+    def timed(step, n, stream=None):
+        stream = stream or inf
+        with torch.cuda.stream(stream):
             step()
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(inf)
+            a.record(stream)
             for _ in range(n):
                 step()
-            b.record(inf)
+            b.record(stream)
         b.synchronize()
         return a, b
 
@@ -329,9 +330,9 @@ def monitor_bench(args, dev):
                 total -= C - (int(lens[m]) - (last - int(seg[m])) * C)
         return total
 
-    def run_monitor(slice_leaves, seconds, ring):
-        """Queue about `seconds` of scans (at the solo rate) back to back; returns (monitor, t0 event, [(end event, bytes)])."""
-        mon = hv.Monitor(wl.msgs, C, ref, alg, slice_leaves, dev, stream=mon_stream, ring=ring)
+    def run_monitor(slice_leaves, ring, stream=None):
+        """Queue ring - 1 scans back to back; returns (monitor, t0 event, [(end event, bytes)])."""
+        mon = hv.Monitor(wl.msgs, C, ref, alg, slice_leaves, dev, stream=stream or mon_stream, ring=ring)
         t0 = torch.cuda.Event(enable_timing=True)
         t0.record(mon.stream)
         ends = []
@@ -353,7 +354,7 @@ def monitor_bench(args, dev):
     for S in args.monitor_slices:
         # the monitor alone at this slice length
         probe = max(8, min(400, int(2 ** 30 * 4 / (S * C)) + 8))
-        mon, t0, ends = run_monitor(S, 0, probe)
+        mon, t0, ends = run_monitor(S, probe)
         ends[-1][0].synchronize()
         ms = t0.elapsed_time(ends[-1][0])
         solo = sum(nb for _, nb in ends) / (ms / 1e3) / 1e9
@@ -363,7 +364,7 @@ def monitor_bench(args, dev):
         for kind, (step, wbytes, flops) in kinds.items():
             window = args.steps * alone[kind] / 1e3
             n_scans = int(2.0 * window * solo * 1e9 / (S * C)) + 8
-            mon, t0, ends = run_monitor(S, window, n_scans + 1)
+            mon, t0, ends = run_monitor(S, n_scans + 1)
             a, b = timed(step, args.steps)
             ends[-1][0].synchronize()
             ta, tb = t0.elapsed_time(a), t0.elapsed_time(b)
@@ -385,6 +386,50 @@ def monitor_bench(args, dev):
             log(f"slice {S}: {kind} {alone[kind]:.2f} -> {co:.2f} ms/step ({slow:+.1f}%), monitor {rate:.0f} GB/s "
                 f"(alone {solo:.0f}), sweep {row[kind]['sweep_s']} s")
         rows.append(row)
+    # spatial partitioning: the monitor on K CUs of its own, the inference work
+    # on a stream masked to the other CUs; slowdowns against the unmasked run.
+    # Each masked stream holds a hardware queue of its own and a process gets
+    # few, so one K per run.
+    n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
+    parts = []
+    for K in [args.monitor_partition] if args.monitor_partition else []:
+        mon_cus = list(range(K))  # low CU numbers, which the runtime spreads over the XCDs
+        rest = [c for c in range(n_cu) if c not in set(mon_cus)]
+        inf_p, mon_p = hv.CuMaskedStream(rest, dev), hv.CuMaskedStream(mon_cus, dev)
+        S = len(mon_cus) * 4 * 64 * 2  # two waves per SIMD of the monitor's CUs
+        probe = 24
+        mon, t0, ends = run_monitor(S, probe, mon_p.stream)
+        ends[-1][0].synchronize()
+        solo = sum(nb for _, nb in ends) / (t0.elapsed_time(ends[-1][0]) / 1e3) / 1e9
+        mon.poll(wait=True)
+        assert mon.mismatches == []
+        part = {"monitor_cus": len(mon_cus), "slice_leaves": S, "monitor_alone_GBps": round(solo, 1)}
+        for kind, (step, wbytes, flops) in kinds.items():
+            a, b = timed(step, args.steps, inf_p.stream)
+            rest_ms = a.elapsed_time(b) / args.steps
+            window = args.steps * rest_ms / 1e3
+            n_scans = int(2.0 * window * solo * 1e9 / (S * C)) + 8
+            mon, t0, ends = run_monitor(S, n_scans + 1, mon_p.stream)
+            a, b = timed(step, args.steps, inf_p.stream)
+            ends[-1][0].synchronize()
+            ta, tb = t0.elapsed_time(a), t0.elapsed_time(b)
+            inside = [nb for e, nb in ends if ta < t0.elapsed_time(e) <= tb]
+            co = a.elapsed_time(b) / args.steps
+            rate = sum(inside) / ((tb - ta) / 1e3) / 1e9
+            mon.poll(wait=True)
+            assert mon.mismatches == []
+            slow = (co / alone[kind] - 1) * 100
+            sweep = pipe.total_bytes / (rate * 1e9) if rate > 0 else None
+            part[kind] = {"alone_ms": round(alone[kind], 3), "on_other_cus_alone_ms": round(rest_ms, 3),
+                          "with_monitor_ms": round(co, 3), "slowdown_pct": round(slow, 2),
+                          "monitor_GBps": round(rate, 1),
+                          "monitor_busy_whole_window": t0.elapsed_time(ends[-1][0]) > tb,
+                          "sweep_s": round(sweep, 3) if sweep else None,
+                          f"avg_slowdown_pct_at_{args.monitor_interval:g}s_interval":
+                              round(slow * min(1.0, sweep / args.monitor_interval), 3) if sweep else None}
+            log(f"{len(mon_cus)} monitor CUs: {kind} {alone[kind]:.2f} -> {rest_ms:.2f} on {len(rest)} CUs alone -> "
+                f"{co:.2f} ms/step with the monitor ({slow:+.1f}%), monitor {rate:.0f} GB/s (alone {solo:.0f})")
+        parts.append(part)  # (the masked streams live until the process ends: torch recorded events on them)
     # a changed byte is found, at its leaf, by one sweep
     rng = np.random.default_rng(W.seed_of(5) + 11)
     m = int(rng.integers(0, len(wl.msgs)))
@@ -409,7 +454,7 @@ def monitor_bench(args, dev):
                                f"decode-shaped (batch {args.decode_batch}, all 560 projections + lm_head) or "
                                "prefill-shaped (2048 tokens, 8 layers) bf16 GEMMs run on the same weights",
                    "hash": alg, "monitor_slice_leaves": pick["slice_leaves"], "monitor_duty": "100% (back to back)",
-                   "changed_byte_detected_at_its_leaf": detected, "slices": rows},
+                   "changed_byte_detected_at_its_leaf": detected, "slices": rows, "partitioned": parts},
     }
     print(json.dumps(line), flush=True)
 
@@ -438,6 +483,8 @@ def main():
     ap.add_argument("--monitor-slices", type=int, nargs="+", default=[1024, 4096, 16384, 65536])
     ap.add_argument("--monitor-slice", type=int, default=4096, help="slice length of the reported value")
     ap.add_argument("--decode-batch", type=int, default=8)
+    ap.add_argument("--monitor-partition", type=int, default=8,
+                    help="monitor CU count for the partitioned run (CU-masked streams; 0: none)")
     ap.add_argument("--monitor-interval", type=float, default=30.0,
                     help="seconds between sweeps for the averaged cost (the paper's runtime-monitoring example)")
     ap.add_argument("--graph", action="store_true",

@@ -83,6 +83,32 @@ hv_status hv_monitor_scan(const hv_monitor_plan* plan, uint64_t first_leaf, uint
                           const uint8_t* ref_digests, uint8_t* slice_digests, uint64_t* result, void* workspace,
                           size_t workspace_bytes, hipStream_t stream);
 
+/* Spatial partitioning for a monitor: a stream whose kernels run only on the
+ * listed compute units (HIP's CU-masked streams), at the default priority.
+ * Giving the monitor a few CUs and the co-running work a stream masked to
+ * the others bounds the monitor's cost to the CUs it takes; sharing CUs
+ * instead slows a co-running kernel by more than the monitor's share, since
+ * that kernel waits for its tiles on the shared CUs.
+ *   mask: host, n_words 32-bit words; bit i of word w selects CU 32*w + i
+ *         in the runtime's numbering (bits at or past the device's CU count
+ *         are ignored).
+ *   stream: host, receives the new stream; release it with hv_stream_destroy.
+ * Errors: HV_ERR_INVALID_ARG for NULL pointers, n_words == 0, or a mask that
+ * selects none of the device's CUs (work on such a stream could never run);
+ * HV_ERR_HIP. */
+hv_status hv_stream_create_cu_masked(const uint32_t* mask, uint32_t n_words, hipStream_t* stream);
+
+/* The CU mask of a stream (n_words words written to mask, host).
+ * Errors: HV_ERR_INVALID_ARG for NULL pointers or n_words == 0; HV_ERR_HIP. */
+hv_status hv_stream_cu_mask(hipStream_t stream, uint32_t* mask, uint32_t n_words);
+
+/* Wait for a stream made by hv_stream_create_cu_masked, then destroy it.
+ * No event recorded on the stream may be queried, waited on or destroyed
+ * afterwards (the runtime's events refer to their stream), so a stream that
+ * other libraries have recorded events on should live until the process ends.
+ * Errors: HV_ERR_INVALID_ARG for a NULL stream; HV_ERR_HIP. */
+hv_status hv_stream_destroy(hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

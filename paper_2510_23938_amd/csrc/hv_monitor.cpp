@@ -130,4 +130,32 @@ hv_status hv_monitor_scan(const hv_monitor_plan* plan, uint64_t first_leaf, uint
     return HV_OK;
 }
 
+hv_status hv_stream_create_cu_masked(const uint32_t* mask, uint32_t n_words, hipStream_t* stream) {
+    if (mask == nullptr || stream == nullptr || n_words == 0)
+        return fail(HV_ERR_INVALID_ARG, "mask and stream must be non-NULL and n_words > 0");
+    int device = 0, n_cu = 0;
+    hipError_t e = hipGetDevice(&device);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess) return hip_fail(e, "device query");
+    uint32_t selected = 0;
+    for (int cu = 0; cu < n_cu && (uint32_t)cu < 32 * n_words; ++cu) selected += (mask[cu / 32] >> (cu % 32)) & 1u;
+    if (selected == 0) return fail(HV_ERR_INVALID_ARG, "the mask selects none of the device's %d compute units", n_cu);
+    if ((e = hipExtStreamCreateWithCUMask(stream, n_words, mask)) != hipSuccess) return hip_fail(e, "stream create");
+    return HV_OK;
+}
+
+hv_status hv_stream_cu_mask(hipStream_t stream, uint32_t* mask, uint32_t n_words) {
+    if (stream == nullptr || mask == nullptr || n_words == 0)
+        return fail(HV_ERR_INVALID_ARG, "stream and mask must be non-NULL and n_words > 0");
+    const hipError_t e = hipExtStreamGetCUMask(stream, n_words, mask);
+    return e == hipSuccess ? HV_OK : hip_fail(e, "stream mask query");
+}
+
+hv_status hv_stream_destroy(hipStream_t stream) {
+    if (stream == nullptr) return fail(HV_ERR_INVALID_ARG, "stream is NULL");
+    hipError_t e = hipStreamSynchronize(stream);
+    if (e == hipSuccess) e = hipStreamDestroy(stream);
+    return e == hipSuccess ? HV_OK : hip_fail(e, "stream destroy");
+}
+
 }  // extern "C"

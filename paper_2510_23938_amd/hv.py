@@ -52,7 +52,8 @@ EXPORTS = (
     "hv_tree_bytes", "hv_tree_build", "hv_tree_update_workspace_bytes", "hv_tree_update",
     "hv_rehash_workspace_bytes", "hv_rehash_chunks",  # include/hv_incremental.h
     "hv_monitor_plan_bytes", "hv_monitor_init", "hv_monitor_scan_workspace_bytes",
-    "hv_monitor_scan",  # include/hv_monitor.h
+    "hv_monitor_scan", "hv_stream_create_cu_masked", "hv_stream_cu_mask",
+    "hv_stream_destroy",  # include/hv_monitor.h
     "hv_plan_bytes", "hv_plan_init", "hv_plan_run",  # include/hv_plan.h
 )
 
@@ -131,6 +132,9 @@ def _load():
         "hv_monitor_init": ([ctypes.c_int, vp, u32, u64, vp, sz, vp, vp], ctypes.c_int),
         "hv_monitor_scan_workspace_bytes": ([ctypes.c_int, u64], sz),
         "hv_monitor_scan": ([vp, u64, u64, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "hv_stream_create_cu_masked": ([vp, u32, vp], ctypes.c_int),
+        "hv_stream_cu_mask": ([vp, vp, u32], ctypes.c_int),
+        "hv_stream_destroy": ([vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -701,6 +705,43 @@ class Monitor:
             self.read += 1
             done += 1
         return done
+
+
+def cu_mask_words(cus, n_cu: int) -> np.ndarray:
+    """The 32-bit mask words selecting compute units ``cus`` of ``n_cu``."""
+    words = np.zeros((n_cu + 31) // 32, dtype=np.uint32)
+    for cu in cus:
+        if not 0 <= cu < n_cu:
+            raise ValueError(f"compute unit {cu} is not in 0..{n_cu - 1}")
+        words[cu // 32] |= np.uint32(1 << (cu % 32))
+    return words
+
+
+class CuMaskedStream:
+    """A stream whose kernels run only on the given compute units
+    (include/hv_monitor.h), usable wherever torch takes a stream.
+
+    The stream lives until the process ends, as torch's own streams do:
+    torch records events on the streams it runs work on (pinned-memory copies,
+    ``torch.cuda.Event``), and those must never outlive their stream.
+    """
+
+    def __init__(self, cus, device="cuda"):
+        self.device = torch.device(device)
+        n_cu = torch.cuda.get_device_properties(self.device).multi_processor_count
+        self.cus = sorted(set(int(c) for c in cus))
+        words = cu_mask_words(self.cus, n_cu)
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(lib.hv_stream_create_cu_masked(words.ctypes.data, len(words), ctypes.byref(handle)))
+        self.handle = handle.value
+        self.stream = torch.cuda.ExternalStream(self.handle, device=self.device)
+
+    def mask(self) -> np.ndarray:
+        n_cu = torch.cuda.get_device_properties(self.device).multi_processor_count
+        words = np.zeros((n_cu + 31) // 32, dtype=np.uint32)
+        _check(lib.hv_stream_cu_mask(self.handle, words.ctypes.data, len(words)))
+        return words
 
 
 def manifest_root(named_tensors, chunk_bytes: int, alg: str = "sha256") -> bytes:

@@ -310,3 +310,17 @@ def test_plan_rejects_before_launch():
     assert run(mk(), exp=0x500000) == hv.HV_ERR_INVALID_ARG            # expected without match
     assert run(mk(), match=0x600000) == hv.HV_ERR_INVALID_ARG          # match without expected
     assert run(mk(), exp=0x500000, match=0x600002) == hv.HV_ERR_INVALID_ARG
+
+
+def test_cu_masked_stream_rejects_before_creating():
+    handle = ctypes.c_void_p()
+    zero = np.zeros(8, dtype=np.uint32)
+    assert hv.lib.hv_stream_create_cu_masked(None, 8, ctypes.byref(handle)) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_stream_create_cu_masked(zero.ctypes.data, 0, ctypes.byref(handle)) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_stream_create_cu_masked(zero.ctypes.data, 8, None) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_stream_cu_mask(None, zero.ctypes.data, 8) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_stream_destroy(None) == hv.HV_ERR_INVALID_ARG
+    w = hv.cu_mask_words([0, 31, 32, 255], 256)
+    assert list(w) == [0x80000001, 1, 0, 0, 0, 0, 0, 0x80000000]
+    with pytest.raises(ValueError):
+        hv.cu_mask_words([256], 256)

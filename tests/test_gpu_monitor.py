@@ -8,6 +8,7 @@ digests of the changed bytes say, slice by slice.  At the full 70B shape: a
 sweep of the untouched set finds nothing, a one-byte change anywhere is found
 at exactly the leaf that holds it, and sampled slices match the oracle.
 """
+import ctypes
 import gc
 import os
 
@@ -186,3 +187,63 @@ def test_70b_sweep_finds_nothing_then_exactly_the_changed_chunk(w70b_monitor):
     mon.scan(leaf - leaf % 16384, min(16384, mon.n_leaves - (leaf - leaf % 16384)))
     mon.poll(wait=True)
     assert mon.mismatches == []
+
+
+def test_cu_masked_raw_stream_scan_then_destroy():
+    # a masked stream used only through the C ABI (no torch event ever
+    # recorded on it): one scan, then the stream is destroyed, which also
+    # frees its hardware queue for the next test
+    n_cu = torch.cuda.get_device_properties(DEV).multi_processor_count
+    lens = np.full(8, 20_000, dtype=np.uint64)
+    buf, host, ptrs, lens, starts = place(lens, 0, seed=905)
+    ref_np = oracle.leaf_digests_mt(host_msgs(host, starts, lens), 4096, 1)
+    ref = torch.from_numpy(ref_np).to(DEV)
+    arr = hv._msg_array(ptrs, lens)
+    plan = hv.hv_monitor_plan()
+    plan_mem = hv.Workspace(DEV).get(hv.lib.hv_monitor_plan_bytes(len(arr)))
+    n = len(ref_np)
+    ws = hv.Workspace(DEV).get(hv.lib.hv_monitor_scan_workspace_bytes(0, n))
+    out = torch.empty_like(ref)
+    result = torch.empty(2, dtype=torch.int64, device=DEV)
+    torch.cuda.synchronize()
+    words = hv.cu_mask_words(range(0, 8), n_cu)
+    handle = ctypes.c_void_p()
+    hv._check(hv.lib.hv_stream_create_cu_masked(words.ctypes.data, len(words), ctypes.byref(handle)))
+    hv._check(hv.lib.hv_monitor_init(0, arr.ctypes.data, len(arr), 4096, plan_mem.data_ptr(), plan_mem.numel(),
+                                     ctypes.byref(plan), handle))
+    hv._check(hv.lib.hv_monitor_scan(ctypes.byref(plan), 0, n, ref.data_ptr(), out.data_ptr(), result.data_ptr(),
+                                     ws.data_ptr(), ws.numel(), handle))
+    hv._check(hv.lib.hv_stream_destroy(handle))  # waits for the scan first
+    assert read(result) == (0, U64_MAX)
+    assert np.array_equal(out.cpu().numpy(), ref_np)
+
+
+def test_cu_masked_streams_with_torch():
+    n_cu = torch.cuda.get_device_properties(DEV).multi_processor_count
+    with pytest.raises(hv.HVError):
+        hv.CuMaskedStream([], DEV)  # a mask with no CU is refused before any stream exists
+    # (the streams live until the process ends: torch records events on them;
+    # each masked stream holds a hardware queue of its own, and a process gets
+    # few of those, so these two are the only masked streams the tests keep)
+    mon_s = hv.CuMaskedStream(range(0, 8), DEV)
+    rest = hv.CuMaskedStream(range(8, n_cu), DEV)
+    assert list(mon_s.mask()) == list(hv.cu_mask_words(range(8), n_cu))
+    assert list(rest.mask()) == list(hv.cu_mask_words(range(8, n_cu), n_cu))
+    lens = np.full(40, 70_000, dtype=np.uint64)
+    buf, host, ptrs, lens, starts = place(lens, 0, seed=904)
+    ref_np = oracle.leaf_digests_mt(host_msgs(host, starts, lens), 4096, threads())
+    ref = torch.from_numpy(ref_np).to(DEV)
+    mon = hv.Monitor((ptrs, lens), 4096, ref, slice_leaves=256, device=DEV, stream=mon_s.stream)
+    out = torch.empty_like(ref)
+    a = torch.randn(1024, 1024, device=DEV)
+    want = a @ a
+    torch.cuda.synchronize()
+    for first in range(0, mon.n_leaves, 256):
+        k = min(256, mon.n_leaves - first)
+        mon.scan(first, k, out[first:first + k])
+    with torch.cuda.stream(rest.stream):
+        got = a @ a
+    mon.poll(wait=True)
+    rest.stream.synchronize()
+    assert mon.mismatches == [] and np.array_equal(out.cpu().numpy(), ref_np)
+    assert torch.allclose(got, want, rtol=1e-5, atol=1e-4)
