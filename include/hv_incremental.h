@@ -61,6 +61,23 @@ hv_status hv_rehash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_b
                            uint32_t n_listed, uint8_t* leaf_digests, void* workspace, size_t workspace_bytes,
                            hipStream_t stream);
 
+/* The four calls above with an explicit hash (hv_alg, as the *_alg calls of
+ * hv.h): with HV_SHA384 every digest and node is 48 bytes (the tree holds
+ * 48-byte nodes, so hv_tree_bytes_alg sizes it for the hash) and the chunk
+ * size of a rehash must be 0 or a multiple of 128.  The plain calls are the
+ * HV_SHA256 case.  A tree must be updated with the hash it was built with.
+ * hv_tree_bytes_alg returns 0 for an unknown algorithm; the others fail with
+ * HV_ERR_INVALID_ARG. */
+size_t hv_tree_bytes_alg(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg);
+hv_status hv_tree_build_alg(hv_alg alg, const uint8_t* leaf_digests, const uint64_t* seg_offsets, uint32_t n_seg,
+                            void* tree, size_t tree_bytes, uint8_t* roots, hipStream_t stream);
+hv_status hv_tree_update_alg(hv_alg alg, const uint8_t* leaf_digests, const uint64_t* seg_offsets, uint32_t n_seg,
+                             void* tree, size_t tree_bytes, const uint64_t* dirty, uint32_t n_dirty, uint8_t* roots,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream);
+hv_status hv_rehash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                               const uint64_t* leaves, uint32_t n_listed, uint8_t* leaf_digests, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

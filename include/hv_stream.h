@@ -38,6 +38,14 @@ hv_status hv_hash_host_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chun
                               uint64_t batch_bytes, void* workspace, size_t workspace_bytes, hipStream_t copy_stream,
                               hipStream_t hash_stream);
 
+/* The same with an explicit hash (hv_alg, as hv_hash_chunks_alg): with
+ * HV_SHA384 the digests are 48 bytes (leaf_digests n_leaves * 48 bytes) and
+ * chunk_bytes must be 0 or a multiple of 128.  The workspace size of
+ * hv_stream_workspace_bytes serves both hashes. */
+hv_status hv_hash_host_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                                  uint8_t* leaf_digests, uint64_t batch_bytes, void* workspace, size_t workspace_bytes,
+                                  hipStream_t copy_stream, hipStream_t hash_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -50,12 +50,12 @@ hv_status check_offsets(const uint64_t* seg_offsets, uint32_t n_seg) {
     return HV_OK;
 }
 
-TreeLayout tree_layout(void* tree, const std::vector<uint64_t>& rows, uint32_t n_seg, uint32_t levels) {
+TreeLayout tree_layout(void* tree, const std::vector<uint64_t>& rows, uint32_t n_seg, uint32_t levels, uint32_t D) {
     Carver c(tree);
     TreeLayout T;
     T.table = c.take<uint64_t>(rows.size());
     const size_t w = (size_t)n_seg + 1;
-    for (uint32_t j = 0; j <= levels; ++j) T.level.push_back(c.take<uint8_t>(rows[j * w + n_seg] * 32));
+    for (uint32_t j = 0; j <= levels; ++j) T.level.push_back(c.take<uint8_t>(rows[j * w + n_seg] * D));
     T.bytes = c.used;
     return T;
 }
@@ -104,20 +104,35 @@ RehashLayout rehash_layout(void* ws, uint32_t n_msgs, uint32_t k) {
     return R;
 }
 
+bool known(hv_alg alg) { return alg == HV_SHA256 || alg == HV_SHA384; }
+uint32_t digest_size(hv_alg alg) { return alg == HV_SHA384 ? 48 : 32; }
+int kernel_alg(hv_alg alg) { return alg == HV_SHA384 ? hv::kAlgSha384 : hv::kAlgSha256; }
+
 }  // namespace
 
 extern "C" {
 
-size_t hv_tree_bytes(const uint64_t* seg_offsets, uint32_t n_seg) {
+size_t hv_tree_bytes_alg(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg) {
+    if (!known(alg)) {
+        (void)fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+        return 0;
+    }
     if (check_offsets(seg_offsets, n_seg) != HV_OK) return 0;
     std::vector<uint64_t> rows;
     uint32_t levels = 0;
     if (!tree_rows(seg_offsets, n_seg, &rows, &levels)) return 0;
-    return tree_layout(nullptr, rows, n_seg, levels).bytes;
+    return tree_layout(nullptr, rows, n_seg, levels, digest_size(alg)).bytes;
 }
 
-hv_status hv_tree_build(const uint8_t* leaf_digests, const uint64_t* seg_offsets, uint32_t n_seg, void* tree,
-                        size_t tree_bytes, uint8_t* roots, hipStream_t stream) {
+size_t hv_tree_bytes(const uint64_t* seg_offsets, uint32_t n_seg) {
+    return hv_tree_bytes_alg(HV_SHA256, seg_offsets, n_seg);
+}
+
+hv_status hv_tree_build_alg(hv_alg alg, const uint8_t* leaf_digests, const uint64_t* seg_offsets, uint32_t n_seg,
+                            void* tree, size_t tree_bytes, uint8_t* roots, hipStream_t stream) {
+    if (!known(alg)) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+    const uint32_t D = digest_size(alg);
+    const int ka = kernel_alg(alg);
     hv_status st = check_offsets(seg_offsets, n_seg);
     if (st != HV_OK) return st;
     const uint64_t n = seg_offsets[n_seg];
@@ -128,30 +143,38 @@ hv_status hv_tree_build(const uint8_t* leaf_digests, const uint64_t* seg_offsets
     std::vector<uint64_t> rows;
     uint32_t levels = 0;
     if (!tree_rows(seg_offsets, n_seg, &rows, &levels)) return fail(HV_ERR_INVALID_ARG, "tree too deep");
-    const TreeLayout need = tree_layout(nullptr, rows, n_seg, levels);
+    const TreeLayout need = tree_layout(nullptr, rows, n_seg, levels, D);
     if (tree == nullptr || tree_bytes < need.bytes)
         return fail(HV_ERR_WORKSPACE, "tree needs %zu bytes, got %zu", need.bytes, tree_bytes);
     if ((uintptr_t)tree % kAlign != 0) return fail(HV_ERR_WORKSPACE, "tree is not 256-byte aligned");
-    const TreeLayout T = tree_layout(tree, rows, n_seg, levels);
+    const TreeLayout T = tree_layout(tree, rows, n_seg, levels, D);
     const size_t w = (size_t)n_seg + 1;
     hipError_t e = hipMemcpyAsync(T.table, rows.data(), rows.size() * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "table upload");
-    if ((e = hv::launch_tree_leaf_level(leaf_digests, n, T.level[0], stream)) != hipSuccess)
+    if ((e = hv::launch_tree_leaf_level(ka, leaf_digests, n, T.level[0], stream)) != hipSuccess)
         return hip_fail(e, "leaf level");
     for (uint32_t j = 0; j < levels; ++j)
-        if ((e = hv::launch_tree_build_level(T.level[j], T.level[j + 1], T.table + j * w, T.table + (j + 1) * w, n_seg,
-                                             rows[(j + 1) * w + n_seg], stream)) != hipSuccess)
+        if ((e = hv::launch_tree_build_level(ka, T.level[j], T.level[j + 1], T.table + j * w, T.table + (j + 1) * w,
+                                             n_seg, rows[(j + 1) * w + n_seg], stream)) != hipSuccess)
             return hip_fail(e, "tree level");
-    if ((e = hv::launch_tree_roots(T.level[levels], T.table + levels * w, n_seg, roots, stream)) != hipSuccess)
+    if ((e = hv::launch_tree_roots(ka, T.level[levels], T.table + levels * w, n_seg, roots, stream)) != hipSuccess)
         return hip_fail(e, "roots");
     return HV_OK;
 }
 
+hv_status hv_tree_build(const uint8_t* leaf_digests, const uint64_t* seg_offsets, uint32_t n_seg, void* tree,
+                        size_t tree_bytes, uint8_t* roots, hipStream_t stream) {
+    return hv_tree_build_alg(HV_SHA256, leaf_digests, seg_offsets, n_seg, tree, tree_bytes, roots, stream);
+}
+
 size_t hv_tree_update_workspace_bytes(uint32_t n_dirty) { return update_layout(nullptr, n_dirty).bytes; }
 
-hv_status hv_tree_update(const uint8_t* leaf_digests, const uint64_t* seg_offsets, uint32_t n_seg, void* tree,
-                         size_t tree_bytes, const uint64_t* dirty, uint32_t n_dirty, uint8_t* roots, void* workspace,
-                         size_t workspace_bytes, hipStream_t stream) {
+hv_status hv_tree_update_alg(hv_alg alg, const uint8_t* leaf_digests, const uint64_t* seg_offsets, uint32_t n_seg,
+                             void* tree, size_t tree_bytes, const uint64_t* dirty, uint32_t n_dirty, uint8_t* roots,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (!known(alg)) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+    const uint32_t D = digest_size(alg);
+    const int ka = kernel_alg(alg);
     hv_status st = check_offsets(seg_offsets, n_seg);
     if (st != HV_OK) return st;
     const uint64_t n = seg_offsets[n_seg];
@@ -163,7 +186,7 @@ hv_status hv_tree_update(const uint8_t* leaf_digests, const uint64_t* seg_offset
     std::vector<uint64_t> rows;
     uint32_t levels = 0;
     if (!tree_rows(seg_offsets, n_seg, &rows, &levels)) return fail(HV_ERR_INVALID_ARG, "tree too deep");
-    const TreeLayout need = tree_layout(nullptr, rows, n_seg, levels);
+    const TreeLayout need = tree_layout(nullptr, rows, n_seg, levels, D);
     if (tree == nullptr || tree_bytes < need.bytes)
         return fail(HV_ERR_WORKSPACE, "tree needs %zu bytes, got %zu", need.bytes, tree_bytes);
     if ((uintptr_t)tree % kAlign != 0) return fail(HV_ERR_WORKSPACE, "tree is not 256-byte aligned");
@@ -171,7 +194,7 @@ hv_status hv_tree_update(const uint8_t* leaf_digests, const uint64_t* seg_offset
     if (workspace == nullptr || workspace_bytes < uneed.bytes)
         return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", uneed.bytes, workspace_bytes);
     if ((uintptr_t)workspace % kAlign != 0) return fail(HV_ERR_WORKSPACE, "workspace is not 256-byte aligned");
-    const TreeLayout T = tree_layout(tree, rows, n_seg, levels);
+    const TreeLayout T = tree_layout(tree, rows, n_seg, levels, D);
     const size_t w = (size_t)n_seg + 1;
     // the offset table is re-sent so the kernels walk exactly the layout planned here
     hipError_t e = hipMemcpyAsync(T.table, rows.data(), rows.size() * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
@@ -183,25 +206,37 @@ hv_status hv_tree_update(const uint8_t* leaf_digests, const uint64_t* seg_offset
             return hip_fail(e, "dirty list upload");
         if ((e = hv::launch_tree_locate(U.dirty, n_dirty, T.table, n_seg, U.seg_of, U.local, stream)) != hipSuccess)
             return hip_fail(e, "locate");
-        if ((e = hv::launch_tree_update_leaves(leaf_digests, U.dirty, n_dirty, T.level[0], stream)) != hipSuccess)
+        if ((e = hv::launch_tree_update_leaves(ka, leaf_digests, U.dirty, n_dirty, T.level[0], stream)) != hipSuccess)
             return hip_fail(e, "leaf update");
         for (uint32_t j = 0; j < levels; ++j)
-            if ((e = hv::launch_tree_update_level(T.level[j], T.level[j + 1], T.table + j * w, T.table + (j + 1) * w,
-                                                  U.seg_of, U.local, n_dirty, j + 1, stream)) != hipSuccess)
+            if ((e = hv::launch_tree_update_level(ka, T.level[j], T.level[j + 1], T.table + j * w,
+                                                  T.table + (j + 1) * w, U.seg_of, U.local, n_dirty, j + 1, stream)) !=
+                hipSuccess)
                 return hip_fail(e, "path update");
     }
-    if ((e = hv::launch_tree_roots(T.level[levels], T.table + levels * w, n_seg, roots, stream)) != hipSuccess)
+    if ((e = hv::launch_tree_roots(ka, T.level[levels], T.table + levels * w, n_seg, roots, stream)) != hipSuccess)
         return hip_fail(e, "roots");
     return HV_OK;
+}
+
+hv_status hv_tree_update(const uint8_t* leaf_digests, const uint64_t* seg_offsets, uint32_t n_seg, void* tree,
+                         size_t tree_bytes, const uint64_t* dirty, uint32_t n_dirty, uint8_t* roots, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+    return hv_tree_update_alg(HV_SHA256, leaf_digests, seg_offsets, n_seg, tree, tree_bytes, dirty, n_dirty, roots,
+                              workspace, workspace_bytes, stream);
 }
 
 size_t hv_rehash_workspace_bytes(uint32_t n_msgs, uint32_t n_listed) {
     return rehash_layout(nullptr, n_msgs, n_listed).bytes;
 }
 
-hv_status hv_rehash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, const uint64_t* leaves,
-                           uint32_t n_listed, uint8_t* leaf_digests, void* workspace, size_t workspace_bytes,
-                           hipStream_t stream) {
+hv_status hv_rehash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                               const uint64_t* leaves, uint32_t n_listed, uint8_t* leaf_digests, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream) {
+    if (!known(alg)) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+    if (alg == HV_SHA384 && chunk_bytes % 128 != 0)
+        return fail(HV_ERR_INVALID_ARG, "chunk_bytes = %llu is not 0 or a multiple of 128 (SHA-384 blocks)",
+                    (unsigned long long)chunk_bytes);
     uint64_t n_leaves = 0, n_full = 0;
     hv_status st = layout(msgs, n_msgs, chunk_bytes, nullptr, &n_leaves, &n_full);
     if (st != HV_OK) return st;
@@ -226,9 +261,17 @@ hv_status hv_rehash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_b
     if ((e = hv::launch_sched_select(L.msgs, L.off, n_msgs, chunk_bytes, R.list, n_listed, L.desc, stream)) !=
         hipSuccess)
         return hip_fail(e, "select kernel");
-    if ((e = hv::launch_sha256_leaves(L.desc, n_listed, n_leaves, leaf_digests, stream)) != hipSuccess)
-        return hip_fail(e, "sha256 leaf kernel");
+    e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.desc, n_listed, n_leaves, leaf_digests, stream)
+                         : hv::launch_sha256_leaves(L.desc, n_listed, n_leaves, leaf_digests, stream);
+    if (e != hipSuccess) return hip_fail(e, "leaf kernel");
     return HV_OK;
+}
+
+hv_status hv_rehash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, const uint64_t* leaves,
+                           uint32_t n_listed, uint8_t* leaf_digests, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream) {
+    return hv_rehash_chunks_alg(HV_SHA256, msgs, n_msgs, chunk_bytes, leaves, n_listed, leaf_digests, workspace,
+                                workspace_bytes, stream);
 }
 
 }  // extern "C"

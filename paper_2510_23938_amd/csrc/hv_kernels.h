@@ -76,17 +76,17 @@ hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const u
                                hipStream_t s);
 
 // Persistent tree for incremental updates (tree.hip).
-hipError_t launch_tree_leaf_level(const uint8_t* digests, uint64_t n, uint8_t* level0, hipStream_t s);
-hipError_t launch_tree_build_level(const uint8_t* in, uint8_t* out, const uint64_t* in_off, const uint64_t* out_off,
-                                   uint32_t n_seg, uint64_t n_out, hipStream_t s);
+hipError_t launch_tree_leaf_level(int alg, const uint8_t* digests, uint64_t n, uint8_t* level0, hipStream_t s);
+hipError_t launch_tree_build_level(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
+                                   const uint64_t* out_off, uint32_t n_seg, uint64_t n_out, hipStream_t s);
 hipError_t launch_tree_locate(const uint64_t* dirty, uint32_t k, const uint64_t* seg_off, uint32_t n_seg,
                               uint32_t* seg_of, uint64_t* local, hipStream_t s);
-hipError_t launch_tree_update_leaves(const uint8_t* digests, const uint64_t* dirty, uint32_t k, uint8_t* level0,
-                                     hipStream_t s);
-hipError_t launch_tree_update_level(const uint8_t* in, uint8_t* out, const uint64_t* in_off, const uint64_t* out_off,
-                                    const uint32_t* seg_of, const uint64_t* local, uint32_t k, uint32_t shift,
-                                    hipStream_t s);
-hipError_t launch_tree_roots(const uint8_t* top, const uint64_t* top_off, uint32_t n_seg, uint8_t* roots,
+hipError_t launch_tree_update_leaves(int alg, const uint8_t* digests, const uint64_t* dirty, uint32_t k,
+                                     uint8_t* level0, hipStream_t s);
+hipError_t launch_tree_update_level(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
+                                    const uint64_t* out_off, const uint32_t* seg_of, const uint64_t* local, uint32_t k,
+                                    uint32_t shift, hipStream_t s);
+hipError_t launch_tree_roots(int alg, const uint8_t* top, const uint64_t* top_off, uint32_t n_seg, uint8_t* roots,
                              hipStream_t s);
 
 // Verification (verify.hip).

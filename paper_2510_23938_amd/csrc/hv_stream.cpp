@@ -134,9 +134,14 @@ size_t hv_stream_workspace_bytes(const hv_msg* msgs, uint32_t n_msgs, uint64_t c
     return stream_layout(nullptr, P, batch_bytes).bytes;
 }
 
-hv_status hv_hash_host_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint8_t* leaf_digests,
-                              uint64_t batch_bytes, void* workspace, size_t workspace_bytes, hipStream_t copy_stream,
-                              hipStream_t hash_stream) {
+hv_status hv_hash_host_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                                  uint8_t* leaf_digests, uint64_t batch_bytes, void* workspace, size_t workspace_bytes,
+                                  hipStream_t copy_stream, hipStream_t hash_stream) {
+    if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+    if (alg == HV_SHA384 && chunk_bytes % 128 != 0)
+        return fail(HV_ERR_INVALID_ARG, "chunk_bytes = %llu is not 0 or a multiple of 128 (SHA-384 blocks)",
+                    (unsigned long long)chunk_bytes);
+    const uint64_t D = alg == HV_SHA384 ? 48 : 32;
     Plan P;
     hv_status st = make_plan(msgs, n_msgs, chunk_bytes, batch_bytes, &P);
     if (st != HV_OK) return st;
@@ -193,10 +198,11 @@ hv_status hv_hash_host_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chun
         st = queue_schedule(L.descs + B.p0, (uint32_t)(B.p1 - B.p0), chunk_bytes, B.n_full, B.n_leaves, L.hash,
                             hash_stream);
         if (st != HV_OK) break;
-        if ((e = hv::launch_sha256_leaves(L.hash.desc, B.n_leaves, B.n_leaves, leaf_digests + 32 * B.first_leaf, hash_stream)) !=
-                hipSuccess ||
-            (e = hipEventRecord(hashed[buf], hash_stream)) != hipSuccess)
-            st = hip_fail(e, "sha256 leaf kernel");
+        uint8_t* out = leaf_digests + D * B.first_leaf;
+        e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.hash.desc, B.n_leaves, B.n_leaves, out, hash_stream)
+                             : hv::launch_sha256_leaves(L.hash.desc, B.n_leaves, B.n_leaves, out, hash_stream);
+        if (e != hipSuccess || (e = hipEventRecord(hashed[buf], hash_stream)) != hipSuccess)
+            st = hip_fail(e, "leaf kernel");
     }
     // every copy was waited on by hash_stream, so this also drains copy_stream's work
     e = hipStreamSynchronize(hash_stream);
@@ -207,6 +213,13 @@ hv_status hv_hash_host_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chun
         if (hashed[i]) (void)hipEventDestroy(hashed[i]);
     }
     return st;
+}
+
+hv_status hv_hash_host_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint8_t* leaf_digests,
+                              uint64_t batch_bytes, void* workspace, size_t workspace_bytes, hipStream_t copy_stream,
+                              hipStream_t hash_stream) {
+    return hv_hash_host_chunks_alg(HV_SHA256, msgs, n_msgs, chunk_bytes, leaf_digests, batch_bytes, workspace,
+                                   workspace_bytes, copy_stream, hash_stream);
 }
 
 }  // extern "C"

@@ -48,9 +48,10 @@ EXPORTS = (
     "hv_compare_roots_alg", "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
     "hv_leaf_schedule",  # include/hv_inspect.h
     "hv_mb_valu", "hv_mb_sha256", "hv_mb_valu64", "hv_mb_sha384", "hv_mb_hbm_read",  # include/hv_microbench.h
-    "hv_stream_workspace_bytes", "hv_hash_host_chunks",  # include/hv_stream.h
+    "hv_stream_workspace_bytes", "hv_hash_host_chunks", "hv_hash_host_chunks_alg",  # include/hv_stream.h
     "hv_tree_bytes", "hv_tree_build", "hv_tree_update_workspace_bytes", "hv_tree_update",
-    "hv_rehash_workspace_bytes", "hv_rehash_chunks",  # include/hv_incremental.h
+    "hv_rehash_workspace_bytes", "hv_rehash_chunks", "hv_tree_bytes_alg", "hv_tree_build_alg",
+    "hv_tree_update_alg", "hv_rehash_chunks_alg",  # include/hv_incremental.h
     "hv_monitor_plan_bytes", "hv_monitor_init", "hv_monitor_scan_workspace_bytes",
     "hv_monitor_scan", "hv_stream_create_cu_masked", "hv_stream_cu_mask",
     "hv_stream_destroy",  # include/hv_monitor.h
@@ -125,6 +126,11 @@ def _load():
         "hv_tree_update": ([vp, vp, u32, vp, sz, vp, u32, vp, vp, sz, vp], ctypes.c_int),
         "hv_rehash_workspace_bytes": ([u32, u32], sz),
         "hv_rehash_chunks": ([vp, u32, u64, vp, u32, vp, vp, sz, vp], ctypes.c_int),
+        "hv_hash_host_chunks_alg": ([ctypes.c_int, vp, u32, u64, vp, u64, vp, sz, vp, vp], ctypes.c_int),
+        "hv_tree_bytes_alg": ([ctypes.c_int, vp, u32], sz),
+        "hv_tree_build_alg": ([ctypes.c_int, vp, vp, u32, vp, sz, vp, vp], ctypes.c_int),
+        "hv_tree_update_alg": ([ctypes.c_int, vp, vp, u32, vp, sz, vp, u32, vp, vp, sz, vp], ctypes.c_int),
+        "hv_rehash_chunks_alg": ([ctypes.c_int, vp, u32, u64, vp, u32, vp, vp, sz, vp], ctypes.c_int),
         "hv_plan_bytes": ([ctypes.c_int, vp, u32, u64, ctypes.c_int], sz),
         "hv_plan_init": ([ctypes.c_int, vp, u32, u64, ctypes.c_int, vp, sz, vp, vp], ctypes.c_int),
         "hv_plan_run": ([vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
@@ -269,9 +275,10 @@ def host_messages_of(arrays) -> tuple:
 
 
 def hv_hash_host_chunks(host_msgs, chunk_bytes: int, batch_bytes: int = 1 << 30, device="cuda",
-                        workspace: Workspace | None = None, copy_stream=None):
+                        workspace: Workspace | None = None, copy_stream=None, alg: str = "sha256"):
     """Leaf digests of host-resident messages streamed through GPU memory
-    (synchronous): ([n_leaves, 32] uint8 device tensor, seg_offsets)."""
+    (synchronous): ([n_leaves, D] uint8 device tensor, seg_offsets)."""
+    code, D = _alg(alg)
     ptrs, lens = host_messages_of(host_msgs) if not (isinstance(host_msgs, tuple) and len(host_msgs) == 2
                                                      and isinstance(host_msgs[0], np.ndarray)) else host_msgs
     seg, n_leaves = hv_leaf_layout(ptrs, lens, chunk_bytes)
@@ -282,10 +289,11 @@ def hv_hash_host_chunks(host_msgs, chunk_bytes: int, batch_bytes: int = 1 << 30,
     if need == 0:
         raise HVError(HV_ERR_INVALID_ARG, lib.hv_last_error().decode("utf-8", "replace"))
     ws = (workspace or Workspace(dev)).get(need)
-    out = torch.empty((n_leaves, 32), dtype=torch.uint8, device=dev)
+    out = torch.empty((n_leaves, D), dtype=torch.uint8, device=dev)
     cs = copy_stream or torch.cuda.Stream(dev)
-    _check(lib.hv_hash_host_chunks(arr.ctypes.data if n else None, n, chunk_bytes, out.data_ptr() if n_leaves else None,
-                                   batch_bytes, ws.data_ptr(), ws.numel(), cs.cuda_stream, _stream(dev)))
+    _check(lib.hv_hash_host_chunks_alg(code, arr.ctypes.data if n else None, n, chunk_bytes,
+                                       out.data_ptr() if n_leaves else None, batch_bytes, ws.data_ptr(), ws.numel(),
+                                       cs.cuda_stream, _stream(dev)))
     return out, seg
 
 
@@ -559,42 +567,48 @@ class Pipeline:
 class Tree:
     """A persistent per-segment Merkle tree on the device (include/hv_incremental.h)."""
 
-    def __init__(self, leaf_digests: torch.Tensor, seg_offsets, roots: torch.Tensor | None = None):
+    def __init__(self, leaf_digests: torch.Tensor, seg_offsets, roots: torch.Tensor | None = None,
+                 alg: str = "sha256"):
+        self.code, D = _alg(alg)
+        self.alg = alg
         self.seg = np.ascontiguousarray(seg_offsets, dtype=np.uint64)
         self.n_seg = len(self.seg) - 1
         self.device = leaf_digests.device
-        nbytes = lib.hv_tree_bytes(self.seg.ctypes.data, self.n_seg)
+        nbytes = lib.hv_tree_bytes_alg(self.code, self.seg.ctypes.data, self.n_seg)
         if nbytes == 0:
             raise HVError(HV_ERR_INVALID_ARG, lib.hv_last_error().decode("utf-8", "replace"))
         self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
-        self.roots = roots if roots is not None else torch.empty((self.n_seg, 32), dtype=torch.uint8,
+        self.roots = roots if roots is not None else torch.empty((self.n_seg, D), dtype=torch.uint8,
                                                                  device=self.device)
         self.ws = Workspace(self.device)
-        _check(lib.hv_tree_build(leaf_digests.data_ptr() if leaf_digests.numel() else None, self.seg.ctypes.data,
-                                 self.n_seg, self.buf.data_ptr(), self.buf.numel(), self.roots.data_ptr(),
-                                 _stream(self.device)))
+        _check(lib.hv_tree_build_alg(self.code, leaf_digests.data_ptr() if leaf_digests.numel() else None,
+                                     self.seg.ctypes.data, self.n_seg, self.buf.data_ptr(), self.buf.numel(),
+                                     self.roots.data_ptr(), _stream(self.device)))
 
     def update(self, leaf_digests: torch.Tensor, dirty) -> torch.Tensor:
         """Recompute the branches above the listed leaves (sorted unique leaf numbers); returns roots."""
         d = np.ascontiguousarray(dirty, dtype=np.uint64)
         ws = self.ws.get(lib.hv_tree_update_workspace_bytes(len(d)))
-        _check(lib.hv_tree_update(leaf_digests.data_ptr() if leaf_digests.numel() else None, self.seg.ctypes.data,
-                                  self.n_seg, self.buf.data_ptr(), self.buf.numel(),
-                                  d.ctypes.data if len(d) else None, len(d), self.roots.data_ptr(),
-                                  ws.data_ptr(), ws.numel(), _stream(self.device)))
+        _check(lib.hv_tree_update_alg(self.code, leaf_digests.data_ptr() if leaf_digests.numel() else None,
+                                      self.seg.ctypes.data, self.n_seg, self.buf.data_ptr(), self.buf.numel(),
+                                      d.ctypes.data if len(d) else None, len(d), self.roots.data_ptr(),
+                                      ws.data_ptr(), ws.numel(), _stream(self.device)))
         return self.roots
 
 
-def hv_rehash_chunks(msgs, chunk_bytes: int, leaves, leaf_digests: torch.Tensor, workspace: Workspace | None = None):
+def hv_rehash_chunks(msgs, chunk_bytes: int, leaves, leaf_digests: torch.Tensor, workspace: Workspace | None = None,
+                     alg: str = "sha256"):
     """Recompute leaf_digests[j] for the listed leaf numbers j (sorted, unique) only."""
+    code, _ = _alg(alg)
     ptrs, lens = _ptr_len(msgs)
     arr = _msg_array(ptrs, lens)
     n = len(arr)
     lst = np.ascontiguousarray(leaves, dtype=np.uint64)
     ws = (workspace or Workspace(leaf_digests.device)).get(lib.hv_rehash_workspace_bytes(n, len(lst)))
-    _check(lib.hv_rehash_chunks(arr.ctypes.data if n else None, n, chunk_bytes, lst.ctypes.data if len(lst) else None,
-                                len(lst), leaf_digests.data_ptr() if leaf_digests.numel() else None,
-                                ws.data_ptr(), ws.numel(), _stream(leaf_digests.device)))
+    _check(lib.hv_rehash_chunks_alg(code, arr.ctypes.data if n else None, n, chunk_bytes,
+                                    lst.ctypes.data if len(lst) else None, len(lst),
+                                    leaf_digests.data_ptr() if leaf_digests.numel() else None,
+                                    ws.data_ptr(), ws.numel(), _stream(leaf_digests.device)))
     return leaf_digests
 
 

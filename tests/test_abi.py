@@ -324,3 +324,23 @@ def test_cu_masked_stream_rejects_before_creating():
     assert list(w) == [0x80000001, 1, 0, 0, 0, 0, 0, 0x80000000]
     with pytest.raises(ValueError):
         hv.cu_mask_words([256], 256)
+
+
+def test_alg_forms_of_streaming_and_incremental_reject_before_launch():
+    seg = np.array([0, 10, 30], dtype=np.uint64)
+    assert hv.lib.hv_tree_bytes_alg(7, seg.ctypes.data, 2) == 0
+    assert hv.lib.hv_tree_bytes_alg(1, seg.ctypes.data, 2) > hv.lib.hv_tree_bytes_alg(0, seg.ctypes.data, 2)
+    assert hv.lib.hv_tree_bytes_alg(0, seg.ctypes.data, 2) == hv.lib.hv_tree_bytes(seg.ctypes.data, 2)
+    assert hv.lib.hv_tree_build_alg(7, 0x1000, seg.ctypes.data, 2, 0x100000, 1 << 20, 0x2000, None) == \
+        hv.HV_ERR_INVALID_ARG
+    d = np.array([1], dtype=np.uint64)
+    assert hv.lib.hv_tree_update_alg(7, 0x1000, seg.ctypes.data, 2, 0x100000, 1 << 20, d.ctypes.data, 1, 0x2000,
+                                     0x200000, 1 << 20, None) == hv.HV_ERR_INVALID_ARG
+    ptrs, lens = _msgs([1000, 64])
+    arr = hv._msg_array(ptrs, lens)
+    st = hv.lib.hv_rehash_chunks_alg(1, arr.ctypes.data, 2, 64, d.ctypes.data, 1, 0x2000, 0x200000, 1 << 20, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"multiple of 128" in hv.lib.hv_last_error()
+    assert hv.lib.hv_rehash_chunks_alg(7, arr.ctypes.data, 2, 64, d.ctypes.data, 1, 0x2000, 0x200000, 1 << 20,
+                                       None) == hv.HV_ERR_INVALID_ARG
+    st = hv.lib.hv_hash_host_chunks_alg(1, arr.ctypes.data, 2, 64, 0x2000, 1 << 20, 0x200000, 1 << 30, None, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"multiple of 128" in hv.lib.hv_last_error()

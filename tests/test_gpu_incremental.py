@@ -70,3 +70,44 @@ def test_update_with_no_change_and_every_leaf():
     torch.cuda.synchronize()
     host = [b.cpu().numpy() for b in bufs]
     assert [bytes(r) for r in roots.cpu().numpy()] == [oracle.seg_root(h, 4096) for h in host]
+
+
+@pytest.mark.parametrize("sizes", [[1], [3], [0, 5, 0], [511, 512, 513], [1000, 1, 7000, 2]])
+def test_tree_build_roots_sha384(sizes):
+    n = int(sum(sizes))
+    entries = W.random_bytes(max(n, 1) * 48, 450 + n, DEV)[: n * 48].view(n, 48)
+    seg = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    tree = hv.Tree(entries, seg, alg="sha384")
+    full = hv.hv_merkle_reduce(entries, seg, alg="sha384")
+    torch.cuda.synchronize()
+    assert tree.roots.shape[1] == 48 and torch.equal(tree.roots, full)
+    host = entries.cpu().numpy()
+    assert [bytes(r) for r in tree.roots.cpu().numpy()] == \
+        [oracle.mth(host[int(seg[s]):int(seg[s + 1])], "sha384") for s in range(len(sizes))]
+
+
+@pytest.mark.parametrize("C", [4096, 128, 0])
+def test_update_after_partial_change_sha384(C):
+    alg = "sha384"
+    rng = np.random.default_rng(C + 384)
+    lens = [0, 100, 4096, 3 * 65536 + 7, 300000, 33]
+    bufs = [W.random_bytes(n, 520 + i, DEV) for i, n in enumerate(lens)]
+    leaves, seg = hv.hv_hash_chunks(bufs, C, alg=alg)
+    tree = hv.Tree(leaves, seg, alg=alg)
+    torch.cuda.synchronize()
+    edits = [(2, 0, 1), (3, lens[3] - 1, lens[3]), (3, 4096 - 3, 4096 + 5)] + \
+        [(4, int(p), int(p) + 1) for p in rng.integers(0, lens[4], 5)]
+    dirty = set()
+    for m, lo, hi in edits:
+        bufs[m][lo:hi] ^= 0x5A
+        dirty.update(int(x) for x in hv.leaves_of_range(seg, C, m, lo, hi))
+    dirty = np.array(sorted(dirty), dtype=np.uint64)
+    hv.hv_rehash_chunks(bufs, C, dirty, leaves, alg=alg)
+    roots = tree.update(leaves, dirty)
+    full_leaves, _ = hv.hv_hash_chunks(bufs, C, alg=alg)
+    full_roots = hv.hv_merkle_reduce(full_leaves, seg, alg=alg)
+    torch.cuda.synchronize()
+    assert torch.equal(leaves, full_leaves)
+    assert torch.equal(roots, full_roots)
+    host = [b.cpu().numpy() for b in bufs]
+    assert [bytes(r) for r in roots.cpu().numpy()] == [oracle.seg_root_alg(h, C, alg) for h in host]

@@ -70,3 +70,18 @@ def test_stream_argument_errors():
         with pytest.raises(hv.HVError) as e:
             hv.hv_hash_host_chunks(msgs, C, batch)
         assert e.value.status == hv.HV_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("C,batch", [(4096, 64 << 10), (128, 8 << 10), (0, 256 << 10)])
+def test_streamed_sha384_equal_resident_and_oracle(C, batch):
+    rng = np.random.default_rng(C + batch + 384)
+    cap = batch if C == 0 else 4 * batch
+    lens = [0, 1, 111, 112, 128, max(C, 1) + 1, batch] + [int(x) for x in rng.integers(0, cap, 10)]
+    msgs = host_messages(lens, 1100, True)
+    got, seg = hv.hv_hash_host_chunks(msgs, C, batch, alg="sha384")
+    resident, seg2 = hv.hv_hash_chunks([m.to(DEV) for m in msgs], C, alg="sha384")
+    torch.cuda.synchronize()
+    assert got.shape[1] == 48 and np.array_equal(seg, seg2)
+    assert torch.equal(got, resident)
+    want = oracle.leaf_digests_mt([m.numpy() for m in msgs], C, 8, "sha384")
+    assert np.array_equal(got.cpu().numpy(), want)
