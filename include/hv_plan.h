@@ -69,6 +69,37 @@ hv_status hv_plan_init(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t
 hv_status hv_plan_run(const hv_verify_plan* plan, uint8_t* leaf_digests, uint8_t* roots, uint8_t* root,
                       const uint8_t* expected, uint32_t* match, hipStream_t stream);
 
+/* Result of hv_verify_model: the paper's verification result (Implementation,
+ * Rust FFI Bridge: a verified flag, the digest and the time taken), with the
+ * root of this path in place of a whole-file digest. */
+typedef struct {
+    int integrity_verified;         /* 1 when the root equals `expected`, else 0 (0 when no expected root) */
+    uint32_t root_bytes;            /* 32 (SHA-256) or 48 (SHA-384) */
+    uint8_t root[48];               /* the root, its first root_bytes bytes */
+    uint64_t verification_time_ns;  /* host wall time of the call */
+} hv_result;
+
+/* Device workspace bytes hv_verify_model needs; 0 (hv_last_error set) for
+ * arguments it would reject. */
+size_t hv_verify_model_workspace_bytes(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                                       int manifest);
+
+/* One call for one verification (synchronous): plan, chunk digests, per-message
+ * roots and the manifest root (manifest = 1; Introduction, hierarchical
+ * integrity verification) or one root over all chunks (manifest = 0), the
+ * comparison with `expected` on the GPU, and the root copied to the host.
+ *   msgs: host array of device messages, as hv_hash_chunks_alg.
+ *   expected: host, 32 or 48 bytes (the hash's digest size), or NULL to only
+ *             compute the root.
+ *   workspace: device, >= hv_verify_model_workspace_bytes(...), 256-byte
+ *             aligned (holds the plan, digests and roots; nothing is kept).
+ *   result: host, filled on HV_OK.
+ * A mismatch is not an error: HV_OK with integrity_verified = 0.
+ * Errors: as hv_plan_init; HV_ERR_INVALID_ARG for a NULL result; HV_ERR_HIP. */
+hv_status hv_verify_model(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, int manifest,
+                          const uint8_t* expected, void* workspace, size_t workspace_bytes, hv_result* result,
+                          hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

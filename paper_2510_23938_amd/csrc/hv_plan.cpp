@@ -2,6 +2,8 @@
 // (message table, leaf table, Merkle launch tables) done once, then runs that
 // only queue kernels on the caller's stream.
 #include <algorithm>
+#include <chrono>
+#include <cstring>
 #include <vector>
 
 #include "hv.h"
@@ -95,6 +97,30 @@ hv_status reduce(hv_alg alg, const uint8_t* in, uint8_t* out, const uint64_t* ta
         in = dst;
     }
     return HV_OK;
+}
+
+// Workspace of hv_verify_model: the plan, then its outputs and the comparison buffers.
+struct ModelLayout {
+    void* plan;
+    uint8_t* leaves;
+    uint8_t* roots;
+    uint8_t* root;
+    uint8_t* expected;
+    uint32_t* match;
+    size_t bytes;
+};
+
+ModelLayout model_layout(void* ws, size_t plan_bytes, uint64_t n_leaves, uint32_t n_seg, uint32_t D) {
+    Carver c(ws);
+    ModelLayout M;
+    M.plan = c.take<uint8_t>(plan_bytes);
+    M.leaves = c.take<uint8_t>(n_leaves * D);
+    M.roots = c.take<uint8_t>((size_t)std::max<uint32_t>(n_seg, 1) * D);
+    M.root = c.take<uint8_t>(D);
+    M.expected = c.take<uint8_t>(D);
+    M.match = c.take<uint32_t>(1);
+    M.bytes = c.used;
+    return M;
 }
 
 }  // namespace
@@ -194,6 +220,61 @@ hv_status hv_plan_run(const hv_verify_plan* plan, uint8_t* leaf_digests, uint8_t
     }
     if (expected != nullptr && (e = hv::launch_verify_root_dev(top, expected, D, match, stream)) != hipSuccess)
         return hip_fail(e, "verify kernel");
+    return HV_OK;
+}
+
+size_t hv_verify_model_workspace_bytes(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                                       int manifest) {
+    Prep p;
+    if (prepare(alg, msgs, n_msgs, chunk_bytes, manifest != 0, &p) != HV_OK) return 0;
+    const uint32_t D = digest_size(alg);
+    const size_t plan_bytes = plan_mem(nullptr, n_msgs, p.n_leaves, p.rows, p.scratch, D).bytes;
+    return model_layout(nullptr, plan_bytes, p.n_leaves, p.n_seg, D).bytes;
+}
+
+hv_status hv_verify_model(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, int manifest,
+                          const uint8_t* expected, void* workspace, size_t workspace_bytes, hv_result* result,
+                          hipStream_t stream) {
+    const auto t0 = std::chrono::steady_clock::now();
+    if (result == nullptr) return fail(HV_ERR_INVALID_ARG, "result is NULL");
+    manifest = manifest != 0;
+    Prep p;
+    hv_status st = prepare(alg, msgs, n_msgs, chunk_bytes, manifest, &p);
+    if (st != HV_OK) return st;
+    const uint32_t D = digest_size(alg);
+    const size_t plan_bytes = plan_mem(nullptr, n_msgs, p.n_leaves, p.rows, p.scratch, D).bytes;
+    const ModelLayout need = model_layout(nullptr, plan_bytes, p.n_leaves, p.n_seg, D);
+    if (workspace == nullptr || workspace_bytes < need.bytes)
+        return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu%s", need.bytes, workspace_bytes,
+                    workspace ? "" : " (NULL)");
+    if ((uintptr_t)workspace % kAlign != 0) return fail(HV_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    const ModelLayout M = model_layout(workspace, plan_bytes, p.n_leaves, p.n_seg, D);
+    hv_verify_plan plan;
+    if ((st = hv_plan_init(alg, msgs, n_msgs, chunk_bytes, manifest, M.plan, plan_bytes, &plan, stream)) != HV_OK)
+        return st;
+    hipError_t e;
+    if (expected != nullptr &&
+        (e = hipMemcpyAsync(M.expected, expected, D, hipMemcpyHostToDevice, stream)) != hipSuccess)
+        return hip_fail(e, "expected root upload");
+    if ((st = hv_plan_run(&plan, M.leaves, M.roots, M.root, expected ? M.expected : nullptr,
+                          expected ? M.match : nullptr, stream)) != HV_OK)
+        return st;
+    uint8_t root[48];
+    uint32_t match = 0;
+    const uint8_t* top = manifest ? M.root : M.roots;
+    if ((e = hipMemcpyAsync(root, top, D, hipMemcpyDeviceToHost, stream)) != hipSuccess)
+        return hip_fail(e, "root copy");
+    if (expected != nullptr && (e = hipMemcpyAsync(&match, M.match, sizeof match, hipMemcpyDeviceToHost, stream)) !=
+                                   hipSuccess)
+        return hip_fail(e, "verdict copy");
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "stream synchronize");
+    *result = hv_result{};
+    result->integrity_verified = expected != nullptr && match == 1 ? 1 : 0;
+    result->root_bytes = D;
+    std::memcpy(result->root, root, D);
+    result->verification_time_ns = (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                                       std::chrono::steady_clock::now() - t0)
+                                       .count();
     return HV_OK;
 }
 

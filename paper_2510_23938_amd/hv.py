@@ -55,7 +55,8 @@ EXPORTS = (
     "hv_monitor_plan_bytes", "hv_monitor_init", "hv_monitor_scan_workspace_bytes",
     "hv_monitor_scan", "hv_stream_create_cu_masked", "hv_stream_cu_mask",
     "hv_stream_destroy",  # include/hv_monitor.h
-    "hv_plan_bytes", "hv_plan_init", "hv_plan_run",  # include/hv_plan.h
+    "hv_plan_bytes", "hv_plan_init", "hv_plan_run", "hv_verify_model_workspace_bytes",
+    "hv_verify_model",  # include/hv_plan.h
 )
 
 
@@ -83,6 +84,11 @@ class hv_verify_plan(ctypes.Structure):
                 ("manifest", ctypes.c_int), ("n_msgs", ctypes.c_uint32), ("n_seg", ctypes.c_uint32),
                 ("chunk_bytes", ctypes.c_uint64), ("n_leaves", ctypes.c_uint64),
                 ("launches", ctypes.c_uint32 * 2), ("tiles", (ctypes.c_uint64 * HV_PLAN_MAX_LAUNCHES) * 2)]
+
+
+class hv_result(ctypes.Structure):
+    _fields_ = [("integrity_verified", ctypes.c_int), ("root_bytes", ctypes.c_uint32),
+                ("root", ctypes.c_uint8 * 48), ("verification_time_ns", ctypes.c_uint64)]
 
 
 class hv_monitor_plan(ctypes.Structure):
@@ -134,6 +140,8 @@ def _load():
         "hv_plan_bytes": ([ctypes.c_int, vp, u32, u64, ctypes.c_int], sz),
         "hv_plan_init": ([ctypes.c_int, vp, u32, u64, ctypes.c_int, vp, sz, vp, vp], ctypes.c_int),
         "hv_plan_run": ([vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
+        "hv_verify_model_workspace_bytes": ([ctypes.c_int, vp, u32, u64, ctypes.c_int], sz),
+        "hv_verify_model": ([ctypes.c_int, vp, u32, u64, ctypes.c_int, vp, vp, sz, vp, vp], ctypes.c_int),
         "hv_monitor_plan_bytes": ([u32], sz),
         "hv_monitor_init": ([ctypes.c_int, vp, u32, u64, vp, sz, vp, vp], ctypes.c_int),
         "hv_monitor_scan_workspace_bytes": ([ctypes.c_int, u64], sz),
@@ -756,6 +764,32 @@ class CuMaskedStream:
         words = np.zeros((n_cu + 31) // 32, dtype=np.uint32)
         _check(lib.hv_stream_cu_mask(self.handle, words.ctypes.data, len(words)))
         return words
+
+
+def verify_model(msgs, chunk_bytes: int, expected: bytes | None = None, alg: str = "sha256",
+                 mode: str = "manifest", device="cuda") -> dict:
+    """One synchronous verification through ``hv_verify_model``: {"integrity_verified",
+    "root" (bytes), "verification_time_ns"}; a mismatch is a False verdict, not an error."""
+    code, D = _alg(alg)
+    if mode not in ("manifest", "single"):
+        raise ValueError(mode)
+    manifest = 1 if mode == "manifest" else 0
+    if expected is not None and len(bytes(expected)) != D:
+        raise ValueError(f"expected root must be {D} bytes for {alg}")
+    ptrs, lens = _ptr_len(msgs)
+    arr = _msg_array(ptrs, lens)
+    n = len(arr)
+    dev = torch.device(device)
+    need = lib.hv_verify_model_workspace_bytes(code, arr.ctypes.data if n else None, n, chunk_bytes, manifest)
+    if need == 0:
+        raise HVError(HV_ERR_INVALID_ARG, lib.hv_last_error().decode("utf-8", "replace"))
+    ws = Workspace(dev).get(need)
+    exp = (ctypes.c_uint8 * D).from_buffer_copy(bytes(expected)) if expected is not None else None
+    res = hv_result()
+    _check(lib.hv_verify_model(code, arr.ctypes.data if n else None, n, chunk_bytes, manifest, exp, ws.data_ptr(),
+                               ws.numel(), ctypes.byref(res), _stream(dev)))
+    return {"integrity_verified": bool(res.integrity_verified), "root": bytes(res.root[:res.root_bytes]),
+            "verification_time_ns": int(res.verification_time_ns)}
 
 
 def manifest_root(named_tensors, chunk_bytes: int, alg: str = "sha256") -> bytes:

@@ -344,3 +344,21 @@ def test_alg_forms_of_streaming_and_incremental_reject_before_launch():
                                        None) == hv.HV_ERR_INVALID_ARG
     st = hv.lib.hv_hash_host_chunks_alg(1, arr.ctypes.data, 2, 64, 0x2000, 1 << 20, 0x200000, 1 << 30, None, None)
     assert st == hv.HV_ERR_INVALID_ARG and b"multiple of 128" in hv.lib.hv_last_error()
+
+
+def test_verify_model_rejects_before_launch():
+    ptrs, lens = _msgs([1000, 64])
+    arr = hv._msg_array(ptrs, lens)
+    p = arr.ctypes.data
+    need = hv.lib.hv_verify_model_workspace_bytes(0, p, 2, 64, 1)
+    assert need > hv.lib.hv_plan_bytes(0, p, 2, 64, 1) and need % 256 == 0
+    assert hv.lib.hv_verify_model_workspace_bytes(5, p, 2, 64, 1) == 0
+    assert hv.lib.hv_verify_model_workspace_bytes(1, p, 2, 64, 1) == 0  # SHA-384 needs 128-byte multiples
+    res = hv.hv_result()
+    call = lambda alg=0, ws=0x100000, wb=need, r=ctypes.byref(res): \
+        hv.lib.hv_verify_model(alg, p, 2, 64, 1, None, ws, wb, r, None)
+    assert call(r=None) == hv.HV_ERR_INVALID_ARG
+    assert call(alg=4) == hv.HV_ERR_INVALID_ARG
+    assert call(wb=need - 1) == hv.HV_ERR_WORKSPACE
+    assert call(ws=None) == hv.HV_ERR_WORKSPACE
+    assert call(ws=0x100010) == hv.HV_ERR_WORKSPACE

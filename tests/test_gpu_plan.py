@@ -103,3 +103,20 @@ def test_graph_replays_track_the_weights(alg):
     other = bytes(48 if alg == "sha384" else 32)
     assert not pipe.replay(other)
     assert pipe.replay(want)
+
+
+@pytest.mark.parametrize("alg,C,mode", [("sha256", 4096, "manifest"), ("sha256", 0, "single"),
+                                        ("sha384", 1024, "manifest"), ("sha384", 128, "single")])
+def test_verify_model_one_call(alg, C, mode):
+    rng = np.random.default_rng(1300)
+    lens = np.concatenate([rng.integers(0, 9000, 40), [0, 1, 200_000]])
+    buf, host, ptrs, lens, starts = place(lens, 1, seed=1301)
+    _, _, want = oracle_roots(host_msgs(host, starts, lens), C, alg, mode)
+    r = hv.verify_model((ptrs, lens), C, want, alg=alg, mode=mode)
+    assert r["root"] == want and r["integrity_verified"] and r["verification_time_ns"] > 0
+    bad = bytearray(want)
+    bad[0] ^= 0x80
+    r = hv.verify_model((ptrs, lens), C, bytes(bad), alg=alg, mode=mode)
+    assert r["root"] == want and not r["integrity_verified"]
+    r = hv.verify_model((ptrs, lens), C, None, alg=alg, mode=mode)
+    assert r["root"] == want and not r["integrity_verified"]
