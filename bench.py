@@ -125,8 +125,23 @@ def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
         n_msgs += 1
         left -= n
         del host
+    # one thread on the first 1 GiB: the oracle's rate per core
+    first = views[0][: min(1 << 30, int(wl.msgs.lens[0]))] if views is not None else \
+        wl.msgs.buffer[: min(1 << 30, int(wl.msgs.offsets[-1] + wl.msgs.lens[-1]))]
+    host = first.cpu().numpy()
+    t0 = time.perf_counter()
+    oracle.leaf_digests_mt([host], C, 1, alg)
+    per_core = host.size / (time.perf_counter() - t0) / 1e9
+    del host
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {
         "value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+        "single_thread_GBps": round(per_core, 4), "host_cpu": model, "host_cpus_visible": os.cpu_count(),
         "sample": f"first {nbytes} bytes ({n_leaves} whole chunks of {n_msgs} message(s)) of this workload, one "
                   f"message at a time; oracle chunk digests on {threads} threads + the Merkle root over them; "
                   f"device-to-host copies not timed",

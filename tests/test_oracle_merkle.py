@@ -3,7 +3,7 @@
 The oracle computes MTH recursively.  These tests check it against:
 * hand expansions of the definition for n = 0..4 written with hashlib;
 * an independent bottom-up construction (pair neighbours, promote an odd last
-  node unchanged) written here with hashlib, for every n up to 600 and
+  node unchanged) written here with hashlib, for every n up to 2000 and
   around powers of two -- the two orders agree only if the split point,
   the prefixes and the operand order are all right;
 * invariants: any single-bit flip changes the root, order matters,
@@ -63,7 +63,7 @@ def test_five_entries_split_at_four_not_duplicated():
 
 def test_recursive_equals_bottom_up_bruteforce():
     pool = rand_entries(4100, 12)
-    sizes = list(range(0, 601)) + [1023, 1024, 1025, 2047, 2048, 2049, 4095, 4097]
+    sizes = list(range(0, 2001)) + [2047, 2048, 2049, 4095, 4097]
     for n in sizes:
         assert oracle.mth(pool[:n]) == bottom_up(pool[:n]), n
 
