@@ -189,17 +189,17 @@ def stream_bench(args, dev):
     copy_stream = torch.cuda.Stream(dev)
 
     def step():
-        leaves, seg = hv.hv_hash_host_chunks(msgs, C, batch, dev, ws, copy_stream)
-        roots = hv.hv_merkle_reduce(leaves, seg)
-        return hv.hv_merkle_reduce(roots, np.array([0, len(msgs)], dtype=np.uint64))
+        leaves, seg = hv.hv_hash_host_chunks(msgs, C, batch, dev, ws, copy_stream, alg=args.alg)
+        roots = hv.hv_merkle_reduce(leaves, seg, alg=args.alg)
+        return hv.hv_merkle_reduce(roots, np.array([0, len(msgs)], dtype=np.uint64), alg=args.alg)
 
     expected = bytes(step().cpu().numpy().reshape(-1))
     for _ in range(args.warmup):
-        assert hv.hv_verify_root(step(), expected)
+        assert hv.hv_verify_root(step(), expected, alg=args.alg)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        assert hv.hv_verify_root(step(), expected)
+        assert hv.hv_verify_root(step(), expected, alg=args.alg)
     torch.cuda.synchronize()
     dt = (time.perf_counter() - t0) / args.steps
     value = total / dt / 1e9
@@ -210,6 +210,7 @@ def stream_bench(args, dev):
         "ms_per_step": round(dt * 1e3, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "u32", "data": "synthetic",
         "config": {"workload": f"first {len(msgs)} tensors of the 70B-shaped bf16 weight set in pinned host memory",
+                   "hash": args.alg,
                    "bytes": total, "chunk_bytes": C, "batch_bytes": batch},
         "roofline": {"bound": "pcie", "achieved": round(value, 3), "peak": round(h2d, 3), "unit": "GB/s",
                      "frac": round(value / h2d, 4), "traffic": None,
@@ -226,14 +227,14 @@ def incremental_bench(args, dev):
     wl = W.workload(args.config, dev)
     C = wl.chunk_bytes
     msgs = wl.msgs
-    leaves, seg = hv.hv_hash_chunks(msgs, C, dev)
-    tree = hv.Tree(leaves, seg)
+    leaves, seg = hv.hv_hash_chunks(msgs, C, dev, alg=args.alg)
+    tree = hv.Tree(leaves, seg, alg=args.alg)
     n_seg = len(seg) - 1
     top_seg = np.array([0, n_seg], dtype=np.uint64)
     rng = np.random.default_rng(W.seed_of(args.config) + 7)
     n_leaves = int(seg[-1])
     k = min(args.incremental, n_leaves)
-    pipe = hv.Pipeline(msgs, C, "manifest", dev)  # full re-verification, for time and for the expected root
+    pipe = hv.Pipeline(msgs, C, "manifest", dev, alg=args.alg)  # full re-verification, time and expected root
     rehash_ws, top_ws = hv.Workspace(dev), hv.Workspace(dev)
     inc_ms, full_ms = [], []
     for rep in range(args.warmup + args.steps):
@@ -249,14 +250,14 @@ def incremental_bench(args, dev):
                 msgs.buffer[o] ^= 0x01
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        hv.hv_rehash_chunks(msgs, C, dirty, leaves, rehash_ws)
+        hv.hv_rehash_chunks(msgs, C, dirty, leaves, rehash_ws, alg=args.alg)
         roots = tree.update(leaves, dirty)
-        top = hv.hv_merkle_reduce(roots, top_seg, top_ws)
+        top = hv.hv_merkle_reduce(roots, top_seg, top_ws, alg=args.alg)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         expected = bytes(pipe.compute().cpu().numpy().reshape(-1))
         t2 = time.perf_counter()
-        assert hv.hv_verify_root(top, expected), "incremental root differs from the full recompute"
+        assert hv.hv_verify_root(top, expected, alg=args.alg), "incremental root differs from the full recompute"
         if rep >= args.warmup:
             inc_ms.append((t1 - t0) * 1e3)
             full_ms.append((t2 - t1) * 1e3)
@@ -267,7 +268,8 @@ def incremental_bench(args, dev):
         "value": round(inc, 4), "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(inc, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
         "dtype": "u32", "data": "synthetic",
-        "config": {"workload": wl.description, "changed_chunks": k, "leaves": n_leaves, "chunk_bytes": C,
+        "config": {"workload": wl.description, "hash": args.alg, "changed_chunks": k, "leaves": n_leaves,
+                   "chunk_bytes": C,
                    "full_reverify_ms": round(full, 3), "speedup": round(full / inc, 2),
                    "matches_full_recompute": True},
     }), flush=True)
@@ -477,8 +479,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=5)
-    ap.add_argument("--alg", choices=sorted(ALGS), default="sha256",
-                    help="hash of chunks and tree nodes (the resident path; --stream and --incremental use sha256)")
+    ap.add_argument("--alg", choices=sorted(ALGS), default="sha256", help="hash of chunks and tree nodes")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-mib", type=int, default=48 << 10,
                     help="bytes of the workload the oracle hashes for cpu_baseline (about 10 s on 16 threads)")
