@@ -37,6 +37,12 @@ OPS_PER_BLOCK = 64 * 14 + 48 * 10 + 8 + 16
 # each; 7 64-bit adds as one v_lshl_add_u64 each), 64 schedule words x
 # (sigma0, sigma1: 8 each; 3 adds), 8 feed-forward adds, 32 byte swaps.
 OPS_PER_BLOCK_384 = 80 * 27 + 64 * 19 + 8 + 32
+# Issue cycles per wave-block if every double-rate instruction (v_bitop3, v_add_u32,
+# v_lshrrev: two per quad-cycle when two waves offer them together) paired up and
+# the others (v_alignbit, v_add3, v_perm, v_lshl_add_u64) took a quad-cycle each:
+# SHA-256 832 x 4 + 568 x 2, SHA-384 2392 x 4 + 1024 x 2.  The bound on the mix
+# that this dual issue allows, beside the one-op-per-lane-cycle peak.
+DUAL_ISSUE_CYCLES = {"sha256": 832 * 4 + 568 * 2, "sha384": 2392 * 4 + 1024 * 2}
 CSRC = "paper_2510_23938_amd/csrc/"
 # per hash: block bytes, length-field bytes, ops per block, leaf kernel, traffic summary, kernel sources
 ALGS = {
@@ -503,6 +509,8 @@ def main():
                     help="seconds between sweeps for the averaged cost (the paper's runtime-monitoring example)")
     ap.add_argument("--graph", action="store_true",
                     help="time HIP-graph replays of the prepared pass (kernel timing from the eager passes)")
+    ap.add_argument("--op-rates", action="store_true",
+                    help="instead: issue rate of each VALU instruction of the SHA mixes (per-op microbenchmark)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 4 GiB device copy first (reference point for HBM byte counters)")
     args = ap.parse_args()
@@ -526,6 +534,16 @@ def main():
         return
     if args.monitor:
         monitor_bench(args, dev)
+        return
+    if args.op_rates:
+        rates = hv.measure_op_rates(dev)
+        lane_cycles = VALU_PEAK_TOPS  # T lane-cycles/s at 2.4 GHz
+        for name, r in rates.items():
+            log(f"{name:16s} {r:7.2f} T lane-ops/s = {r / lane_cycles:.2f} per lane per cycle at 2.4 GHz")
+        print(json.dumps({"metric": "VALU issue rate per instruction (8 independent chains, full occupancy), 1 MI355X",
+                          "unit": "T lane-ops/s", "rates": {k: round(v, 2) for k, v in rates.items()},
+                          "per_lane_cycle_at_2.4GHz": {k: round(v / lane_cycles, 3) for k, v in rates.items()}}),
+              flush=True)
         return
     if args.copy_calibration:
         a = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
@@ -603,6 +621,9 @@ def main():
             "kernel_ms": round(k_ms, 3), "ops_per_block": ops_per_block,
             "hashed_GBps": round(total / k_ms / 1e6, 2),
             "roof_GBps": round(VALU_PEAK_TOPS * 1e12 / ops_per_block * block_bytes / 1e9, 1),
+            "dual_issue_bound_GBps": round(1024 * 64 * 2.4e9 / DUAL_ISSUE_CYCLES[alg] * block_bytes / 1e9, 1),
+            "frac_of_dual_issue_bound": round(total / k_ms / 1e6 / (1024 * 64 * 2.4e9 / DUAL_ISSUE_CYCLES[alg]
+                                                                    * block_bytes / 1e9), 4),
         },
     }
     if not args.no_peaks:

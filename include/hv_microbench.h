@@ -49,6 +49,18 @@ hv_status hv_mb_valu64(uint32_t* sink, uint32_t grid, uint32_t iters, uint64_t* 
 hv_status hv_mb_sha384(uint32_t* sink, uint32_t grid, uint32_t blocks, uint64_t* blocks_per_launch,
                        hipStream_t stream);
 
+/* Issue rate of one VALU instruction: eight independent chains per lane of
+ *   op 0 v_alignbit_b32, 1 v_bitop3_b32, 2 v_add3_u32, 3 v_add_u32,
+ *   4 v_xor_b32, 5 v_lshrrev_b32, 6 v_perm_b32, 7 v_lshl_add_u64,
+ * 32 instructions per loop trip (four of each of the eight chains), `iters`
+ * trips, `grid` blocks of 256 lanes.  Some of these issue
+ * two per quad-cycle when two waves of a SIMD offer them together; comparing
+ * the rates shows which.
+ *   ops_per_launch: host, receives grid * 256 * iters * 32.
+ * Errors: HV_ERR_INVALID_ARG for NULL pointers, grid == 0 or op > 7; HV_ERR_HIP. */
+hv_status hv_mb_op_rate(uint32_t op, uint32_t* sink, uint32_t grid, uint32_t iters, uint64_t* ops_per_launch,
+                        hipStream_t stream);
+
 /* Streaming read of `nbytes` (a multiple of 16) at `buf` with 16-byte loads,
  * grid-stride, folded to one word per lane.
  *   buf: device, 16-byte aligned.   sink: device, grid * 256 uint32.

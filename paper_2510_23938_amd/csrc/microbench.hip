@@ -103,6 +103,71 @@ __global__ void __launch_bounds__(kThreads) sha256_registers_kernel(uint32_t* __
     sink[tid] = r;
 }
 
+// Issue rate of one instruction: eight independent chains per lane, four
+// trips of the eight per loop iteration, written as inline assembly so that
+// the compiler neither fuses (two adds into v_add3) nor splits them.
+constexpr int kOpKinds = 8;  // alignbit, bitop3, add3, add, xor, lshr, perm, lshl_add_u64
+
+#define HV_CHAIN8(S) S(0) S(1) S(2) S(3) S(4) S(5) S(6) S(7)
+
+template <int OP>
+__global__ void __launch_bounds__(kThreads) op_rate_kernel(uint32_t* __restrict__ sink, uint32_t iters) {
+    const uint32_t tid = blockIdx.x * kThreads + threadIdx.x;
+    uint32_t x[kChains];
+    uint64_t w[kChains];
+#pragma unroll
+    for (int k = 0; k < kChains; ++k) {
+        x[k] = tid * 0x9E3779B9u + (uint32_t)k;
+        w[k] = hv::pack(tid, (uint32_t)k);
+    }
+    const uint32_t y = tid ^ 0x01234567u, z = tid + 0x5bd1e995u;
+    const uint64_t y64 = hv::pack(y, z);
+    for (uint32_t it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int rep = 0; rep < 4; ++rep) {
+            if constexpr (OP == 0) {
+#define S(k) asm volatile("v_alignbit_b32 %0, %0, %1, 7" : "+v"(x[k]) : "v"(y));
+                HV_CHAIN8(S)
+#undef S
+            } else if constexpr (OP == 1) {
+#define S(k) asm volatile("v_bitop3_b32 %0, %0, %1, %2 bitop3:0x96" : "+v"(x[k]) : "v"(y), "v"(z));
+                HV_CHAIN8(S)
+#undef S
+            } else if constexpr (OP == 2) {
+#define S(k) asm volatile("v_add3_u32 %0, %0, %1, %2" : "+v"(x[k]) : "v"(y), "v"(z));
+                HV_CHAIN8(S)
+#undef S
+            } else if constexpr (OP == 3) {
+#define S(k) asm volatile("v_add_u32_e32 %0, %0, %1" : "+v"(x[k]) : "v"(y));
+                HV_CHAIN8(S)
+#undef S
+            } else if constexpr (OP == 4) {
+#define S(k) asm volatile("v_xor_b32_e32 %0, %0, %1" : "+v"(x[k]) : "v"(y));
+                HV_CHAIN8(S)
+#undef S
+            } else if constexpr (OP == 5) {
+#define S(k) asm volatile("v_lshrrev_b32_e32 %0, 3, %0" : "+v"(x[k]));
+                HV_CHAIN8(S)
+#undef S
+            } else if constexpr (OP == 6) {
+#define S(k) asm volatile("v_perm_b32 %0, %0, %1, %2" : "+v"(x[k]) : "v"(y), "v"(z));
+                HV_CHAIN8(S)
+#undef S
+            } else {
+#define S(k) asm volatile("v_lshl_add_u64 %0, %0, 0, %1" : "+v"(w[k]) : "v"(y64));
+                HV_CHAIN8(S)
+#undef S
+            }
+        }
+    }
+    uint32_t r = 0;
+#pragma unroll
+    for (int k = 0; k < kChains; ++k) r ^= x[k] ^ hv::hi32(w[k]) ^ hv::lo32(w[k]);
+    sink[tid] = r;
+}
+
+#undef HV_CHAIN8
+
 // SHA-384 compressions on registers only (section 6.4 rounds), as above.
 __global__ void __launch_bounds__(kThreads) sha384_registers_kernel(uint32_t* __restrict__ sink, uint32_t blocks) {
     const uint32_t tid = blockIdx.x * kThreads + threadIdx.x;
@@ -154,6 +219,24 @@ hv_status hv_mb_sha384(uint32_t* sink, uint32_t grid, uint32_t blocks, uint64_t*
     if (sink == nullptr || blocks_per_launch == nullptr || grid == 0) return HV_ERR_INVALID_ARG;
     sha384_registers_kernel<<<grid, kThreads, 0, stream>>>(sink, blocks);
     *blocks_per_launch = (uint64_t)grid * kThreads * blocks;
+    return hipGetLastError() == hipSuccess ? HV_OK : HV_ERR_HIP;
+}
+
+hv_status hv_mb_op_rate(uint32_t op, uint32_t* sink, uint32_t grid, uint32_t iters, uint64_t* ops_per_launch,
+                        hipStream_t stream) {
+    if (sink == nullptr || ops_per_launch == nullptr || grid == 0 || op >= (uint32_t)kOpKinds)
+        return HV_ERR_INVALID_ARG;
+    switch (op) {
+        case 0: op_rate_kernel<0><<<grid, kThreads, 0, stream>>>(sink, iters); break;
+        case 1: op_rate_kernel<1><<<grid, kThreads, 0, stream>>>(sink, iters); break;
+        case 2: op_rate_kernel<2><<<grid, kThreads, 0, stream>>>(sink, iters); break;
+        case 3: op_rate_kernel<3><<<grid, kThreads, 0, stream>>>(sink, iters); break;
+        case 4: op_rate_kernel<4><<<grid, kThreads, 0, stream>>>(sink, iters); break;
+        case 5: op_rate_kernel<5><<<grid, kThreads, 0, stream>>>(sink, iters); break;
+        case 6: op_rate_kernel<6><<<grid, kThreads, 0, stream>>>(sink, iters); break;
+        default: op_rate_kernel<7><<<grid, kThreads, 0, stream>>>(sink, iters); break;
+    }
+    *ops_per_launch = (uint64_t)grid * kThreads * iters * 4 * kChains;
     return hipGetLastError() == hipSuccess ? HV_OK : HV_ERR_HIP;
 }
 

@@ -47,7 +47,8 @@ EXPORTS = (
     "hv_hash_chunks_alg", "hv_merkle_workspace_bytes_alg", "hv_merkle_reduce_alg", "hv_verify_root_alg",
     "hv_compare_roots_alg", "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
     "hv_leaf_schedule",  # include/hv_inspect.h
-    "hv_mb_valu", "hv_mb_sha256", "hv_mb_valu64", "hv_mb_sha384", "hv_mb_hbm_read",  # include/hv_microbench.h
+    "hv_mb_valu", "hv_mb_sha256", "hv_mb_valu64", "hv_mb_sha384", "hv_mb_op_rate",
+    "hv_mb_hbm_read",  # include/hv_microbench.h
     "hv_stream_workspace_bytes", "hv_hash_host_chunks", "hv_hash_host_chunks_alg",  # include/hv_stream.h
     "hv_tree_bytes", "hv_tree_build", "hv_tree_update_workspace_bytes", "hv_tree_update",
     "hv_rehash_workspace_bytes", "hv_rehash_chunks", "hv_tree_bytes_alg", "hv_tree_build_alg",
@@ -124,6 +125,7 @@ def _load():
         "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_valu64": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_sha384": ([vp, u32, u32, vp, vp], ctypes.c_int),
+        "hv_mb_op_rate": ([u32, vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_stream_workspace_bytes": ([vp, u32, u64, u64], sz),
         "hv_hash_host_chunks": ([vp, u32, u64, vp, u64, vp, sz, vp, vp], ctypes.c_int),
         "hv_tree_bytes": ([vp, u32], sz),
@@ -411,6 +413,32 @@ def measure_sha256_ceiling(device="cuda", grid=8192, blocks=256, reps=5, alg: st
         best = ms if best is None else min(best, ms)
     return {"blocks_per_s": n.value / (best / 1e3), "GBps_equiv": n.value * block_bytes / (best / 1e3) / 1e9,
             "ms": best, "blocks": n.value}
+
+
+OP_RATE_NAMES = ("v_alignbit_b32", "v_bitop3_b32", "v_add3_u32", "v_add_u32", "v_xor_b32", "v_lshrrev_b32",
+                 "v_perm_b32", "v_lshl_add_u64")
+
+
+def measure_op_rates(device="cuda", grid=16384, iters=1024, reps=5) -> dict:
+    """Best issue rate (T lane-ops/s) of each instruction of OP_RATE_NAMES."""
+    dev = torch.device(device)
+    sink = torch.empty(grid * 256, dtype=torch.int32, device=dev)
+    ops = ctypes.c_uint64(0)
+    s = _stream(dev)
+    out = {}
+    for op, name in enumerate(OP_RATE_NAMES):
+        _check(lib.hv_mb_op_rate(op, sink.data_ptr(), grid, 8, ctypes.byref(ops), s))  # warm-up
+        best = None
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            _check(lib.hv_mb_op_rate(op, sink.data_ptr(), grid, iters, ctypes.byref(ops), s))
+            b.record()
+            b.synchronize()
+            ms = a.elapsed_time(b)
+            best = ms if best is None else min(best, ms)
+        out[name] = ops.value / (best / 1e3) / 1e12
+    return out
 
 
 def measure_hbm_read(nbytes=16 << 30, device="cuda", grid=None, reps=5) -> dict:
