@@ -137,3 +137,15 @@ def test_verify_and_compare():
     b[9, 31] ^= 128
     mism = hv.hv_compare_roots(a, b).cpu().numpy()
     assert list(np.nonzero(mism)[0]) == [3, 9]
+
+
+@pytest.mark.parametrize("alg", ["sha256", "sha384"])
+@pytest.mark.parametrize("align_off", [0, 5])
+def test_single_long_chunk(alg, align_off):
+    # one 48 MiB + 17 byte message as one chunk: one lane runs ~786K dependent
+    # blocks (the long-loop and tail paths of both load paths)
+    n = (48 << 20) + 17
+    buf, host, ptrs, lens, starts = place([n], align_off, seed=77)
+    leaves, _ = hv.hv_hash_chunks((ptrs, lens), 0, DEV, alg=alg)
+    torch.cuda.synchronize()
+    assert bytes(leaves.cpu().numpy()[0]) == oracle.digest(host[int(starts[0]):int(starts[0]) + n].tobytes(), alg)
