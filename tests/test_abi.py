@@ -362,3 +362,18 @@ def test_verify_model_rejects_before_launch():
     assert call(wb=need - 1) == hv.HV_ERR_WORKSPACE
     assert call(ws=None) == hv.HV_ERR_WORKSPACE
     assert call(ws=0x100010) == hv.HV_ERR_WORKSPACE
+
+
+def test_headers_compile_as_c_and_the_c_client_links(tmp_path):
+    # the C client (tests/c_client) uses only include/*.h and the HIP runtime:
+    # compile it as strict C11 with warnings as errors and link it against libhv
+    import subprocess
+
+    c_dir = os.path.join(ROOT, "tests", "c_client")
+    exe = tmp_path / "verify_example"
+    pkg = os.path.join(ROOT, "paper_2510_23938_amd")
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include", os.path.join(c_dir, "verify_example.c"),
+           "-o", str(exe), "-L", pkg, "-lhv", "-L", "/opt/rocm/lib", "-lamdhip64"]
+    subprocess.run(cmd, check=True, capture_output=True)
+    assert exe.exists()
