@@ -507,6 +507,8 @@ def main():
                     help="monitor CU count for the partitioned run (CU-masked streams; 0: none)")
     ap.add_argument("--monitor-interval", type=float, default=30.0,
                     help="seconds between sweeps for the averaged cost (the paper's runtime-monitoring example)")
+    ap.add_argument("--leaf-kernel", choices=["auto", "one-wave", "two-wave", "two-wave-compact"], default="auto",
+                    help="SHA-256 leaf kernel (auto: the two-wave kernel for at most 128 leaves per CU)")
     ap.add_argument("--graph", action="store_true",
                     help="time HIP-graph replays of the prepared pass (kernel timing from the eager passes)")
     ap.add_argument("--op-rates", action="store_true",
@@ -526,6 +528,7 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    hv.set_leaf_kernel(args.leaf_kernel)
     if args.stream > 0:
         stream_bench(args, dev)
         return
@@ -612,6 +615,7 @@ def main():
             "leaves": pipe.n_leaves, "chunk_bytes": wl.chunk_bytes, "hash": alg, f"{alg}_blocks": blocks,
             "verified": True, "mismatch_detected": negative_ok,
             "step": "HIP graph replay of the prepared pass" if args.graph else "prepared pass, eager launches",
+            "leaf_kernel": args.leaf_kernel,
             "eager_ms_per_step": round(eager_ms, 3),
         },
         "roofline": {

@@ -26,6 +26,19 @@ extern "C" {
 hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t* table,
                            void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Leaf-kernel choice for tests and measurements, per calling thread:
+ * 0 = automatic (SHA-256 calls with at most 128 leaves per compute unit of
+ * the current device -- 32768 on MI355X -- use the two-wave kernel, which
+ * moves the message schedule to a second wave and shortens each chunk's chain
+ * of blocks; others use the one-wave kernel), 1 = always the
+ * one-wave kernel, 2 = always the two-wave kernel, 3 = always the two-wave
+ * kernel with two producer/consumer pairs per workgroup (the layout it takes
+ * above 64 leaves per compute unit).  Monitor scans (hv_monitor.h) take the
+ * one-wave kernel under the automatic choice.  The digests do not depend on
+ * it.  SHA-384 has one kernel.
+ * Errors: HV_ERR_INVALID_ARG for another value. */
+hv_status hv_set_leaf_kernel(int choice);
+
 #ifdef __cplusplus
 }
 #endif

@@ -89,6 +89,7 @@ struct Timing {
     hipEvent_t start = nullptr, stop = nullptr;
 };
 thread_local Timing g_timing;
+thread_local int g_leaf_kernel = 0;
 
 constexpr int kMaxLaunches = kMaxMerkleLaunches;
 
@@ -226,7 +227,7 @@ hv_status hv_hash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, ui
 
     if ((st = leaf_timing_start(stream)) != HV_OK) return st;
     const hipError_t e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream)
-                                          : hv::launch_sha256_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream);
+                                          : hv::launch_sha256_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream);
     if (e != hipSuccess) return hip_fail(e, "leaf kernel");
     return leaf_timing_stop(stream);
 }
@@ -358,6 +359,10 @@ hv_status hv_compare_roots(const uint8_t* roots, const uint8_t* expected, uint32
 
 }  // extern "C"
 
+namespace hv {
+int leaf_kernel_choice() { return g_leaf_kernel; }
+}  // namespace hv
+
 namespace hvh {
 
 hv_status leaf_timing_start(hipStream_t stream) {
@@ -382,6 +387,12 @@ hv_status leaf_timing_stop(hipStream_t stream) {
 }  // namespace hvh
 
 extern "C" {
+
+hv_status hv_set_leaf_kernel(int choice) {
+    if (choice < 0 || choice > 3) return fail(HV_ERR_INVALID_ARG, "leaf kernel choice %d is not 0, 1, 2 or 3", choice);
+    g_leaf_kernel = choice;
+    return HV_OK;
+}
 
 hv_status hv_set_kernel_timing(int enable) {
     g_timing.enabled = enable != 0;

@@ -63,6 +63,22 @@ hipError_t launch_sched_range(const MsgDesc* msgs, const Pair* off, uint32_t n, 
 // result[1] = min(result[1], lowest mismatching leaf number).  D is 32 or 48.
 hipError_t launch_monitor_compare(const uint8_t* digests, const uint8_t* ref, uint64_t first, uint64_t k, uint32_t D,
                                   uint64_t* result, hipStream_t s);
+// The two-wave SHA-256 leaf kernel (sha256_split.hip; same contract as
+// launch_sha256_leaves), with one or two producer/consumer pairs per
+// workgroup.  The automatic choice takes it for up to 128 leaves per compute
+// unit of the current device (32768 on a 256-CU device).
+hipError_t launch_sha256_split(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
+                               bool two_pairs, hipStream_t s);
+// Leaf-kernel choice of the calling thread (hv_set_leaf_kernel): 0 automatic,
+// 1 one-wave kernel, 2 two-wave kernel, 3 two-wave kernel with two pairs per
+// workgroup.
+int leaf_kernel_choice();
+// SHA-256 leaf digests with the kernel that choice selects (the callers' entry).
+// background: work that shares the chip with other work (monitor scans);
+// under the automatic choice it takes the one-wave kernel, which hashes a byte
+// in the least CU time, rather than the one with the shortest chains.
+hipError_t launch_sha256_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
+                              hipStream_t s, bool background = false);
 hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                                 hipStream_t s);
 

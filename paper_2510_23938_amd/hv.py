@@ -46,7 +46,7 @@ EXPORTS = (
     "hv_merkle_reduce", "hv_verify_workspace_bytes", "hv_verify_root", "hv_compare_roots",
     "hv_hash_chunks_alg", "hv_merkle_workspace_bytes_alg", "hv_merkle_reduce_alg", "hv_verify_root_alg",
     "hv_compare_roots_alg", "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
-    "hv_leaf_schedule",  # include/hv_inspect.h
+    "hv_leaf_schedule", "hv_set_leaf_kernel",  # include/hv_inspect.h
     "hv_mb_valu", "hv_mb_sha256", "hv_mb_valu64", "hv_mb_sha384", "hv_mb_op_rate",
     "hv_mb_hbm_read",  # include/hv_microbench.h
     "hv_stream_workspace_bytes", "hv_hash_host_chunks", "hv_hash_host_chunks_alg",  # include/hv_stream.h
@@ -120,6 +120,7 @@ def _load():
         "hv_set_kernel_timing": ([ctypes.c_int], ctypes.c_int),
         "hv_leaf_kernel_ms": ([vp], ctypes.c_int),
         "hv_leaf_schedule": ([vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
+        "hv_set_leaf_kernel": ([ctypes.c_int], ctypes.c_int),
         "hv_mb_valu": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_hbm_read": ([vp, u64, vp, u32, vp], ctypes.c_int),
         "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
@@ -461,6 +462,12 @@ def measure_hbm_read(nbytes=16 << 30, device="cuda", grid=None, reps=5) -> dict:
         best = ms if best is None else min(best, ms)
     del buf
     return {"GBps": nbytes / (best / 1e3) / 1e9, "ms": best, "bytes": nbytes, "grid": grid}
+
+
+def set_leaf_kernel(choice: str):
+    """SHA-256 leaf kernel for this thread: "auto", "one-wave", "two-wave" or "two-wave-compact" (two
+    producer/consumer pairs per workgroup); digests do not depend on it."""
+    _check(lib.hv_set_leaf_kernel({"auto": 0, "one-wave": 1, "two-wave": 2, "two-wave-compact": 3}[choice]))
 
 
 def set_kernel_timing(enable: bool):

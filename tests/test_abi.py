@@ -377,3 +377,12 @@ def test_headers_compile_as_c_and_the_c_client_links(tmp_path):
            "-o", str(exe), "-L", pkg, "-lhv", "-L", "/opt/rocm/lib", "-lamdhip64"]
     subprocess.run(cmd, check=True, capture_output=True)
     assert exe.exists()
+
+
+def test_leaf_kernel_choice_is_validated():
+    for bad in (-1, 4):
+        assert hv.lib.hv_set_leaf_kernel(bad) == hv.HV_ERR_INVALID_ARG
+    for ok in (1, 2, 3, 0):
+        assert hv.lib.hv_set_leaf_kernel(ok) == hv.HV_OK
+    with pytest.raises(KeyError):
+        hv.set_leaf_kernel("fast")

@@ -149,3 +149,74 @@ def test_single_long_chunk(alg, align_off):
     leaves, _ = hv.hv_hash_chunks((ptrs, lens), 0, DEV, alg=alg)
     torch.cuda.synchronize()
     assert bytes(leaves.cpu().numpy()[0]) == oracle.digest(host[int(starts[0]):int(starts[0]) + n].tobytes(), alg)
+
+
+@pytest.fixture
+def leaf_kernel():
+    yield hv.set_leaf_kernel
+    hv.set_leaf_kernel("auto")
+
+
+@pytest.mark.parametrize("choice", ["one-wave", "two-wave", "two-wave-compact"])
+@pytest.mark.parametrize("align_off", [0, 3])
+@pytest.mark.parametrize("C", [64, 4096, 0])
+def test_both_sha256_leaf_kernels(C, align_off, choice, leaf_kernel):
+    # the one-wave kernel and the two-wave kernel (message schedule on a second
+    # wave) forced on the same inputs, every length 0..1100
+    leaf_kernel(choice)
+    lens = np.arange(0, 1101)
+    buf, host, ptrs, lens, starts = place(lens, align_off, seed=150 + align_off)
+    check_all(buf, host, ptrs, lens, starts, C, f"{choice} C={C} off={align_off}")
+
+
+@pytest.mark.parametrize("choice", ["one-wave", "two-wave", "two-wave-compact"])
+@pytest.mark.parametrize("C", [64, 0])
+def test_both_kernels_mixed_alignment(C, choice, leaf_kernel):
+    # every message at its own offset 0..15 from a 16-byte boundary, so waves
+    # mix aligned and unaligned chunks (the kernels choose a load path per wave)
+    leaf_kernel(choice)
+    rng = np.random.default_rng(152)
+    lens = np.concatenate([np.arange(0, 300), rng.integers(300, 5000, 200)]).astype(np.uint64)
+    offs = (np.arange(len(lens)) * 7) % 16
+    starts = np.zeros(len(lens), dtype=np.uint64)
+    pos = 0
+    for i, n in enumerate(lens):
+        starts[i] = pos + offs[i]
+        pos += (int(n) + int(offs[i]) + 16 + 15) // 16 * 16
+    buf = W.random_bytes(pos, 153, DEV)
+    host = buf.cpu().numpy()
+    ptrs = np.uint64(buf.data_ptr()) + starts
+    ptrs[lens == 0] = 0
+    check_all(buf, host, ptrs, lens, starts, C, f"{choice} mixed C={C}")
+
+
+@pytest.mark.parametrize("choice", ["auto", "two-wave"])
+def test_two_wave_kernel_two_pairs(choice, leaf_kernel):
+    # more than 64 chunks per CU: the two-wave kernel runs two producer/consumer
+    # pairs per workgroup; random lengths and offsets give the pairs of a
+    # workgroup different block counts and load paths
+    leaf_kernel(choice)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 100 * cus
+    rng = np.random.default_rng(154)
+    lens = rng.integers(0, 1500, n).astype(np.uint64)
+    lens[rng.integers(0, n, 40)] = rng.integers(20000, 70000, 40).astype(np.uint64)
+    offs = rng.integers(0, 16, n) * (rng.random(n) < 0.1)
+    starts = np.zeros(n, dtype=np.uint64)
+    pos = 0
+    for i, L in enumerate(lens):
+        starts[i] = pos + offs[i]
+        pos += (int(L) + int(offs[i]) + 16 + 15) // 16 * 16
+    buf = W.random_bytes(pos, 155, DEV)
+    host = buf.cpu().numpy()
+    ptrs = np.uint64(buf.data_ptr()) + starts
+    ptrs[lens == 0] = 0
+    check_all(buf, host, ptrs, lens, starts, 0, f"{choice} two pairs n={n}")
+
+
+@pytest.mark.parametrize("choice", ["one-wave", "two-wave"])
+def test_both_kernels_long_chunks(choice, leaf_kernel):
+    leaf_kernel(choice)
+    lens = [(8 << 20) + 55, (8 << 20) + 56, 3 << 20, 1, 0]
+    buf, host, ptrs, lens, starts = place(lens, 0, seed=151)
+    check_all(buf, host, ptrs, lens, starts, 0, f"{choice} long")
