@@ -168,6 +168,54 @@ __device__ __forceinline__ void produce_all(uint64_t src, uint64_t total, uint32
     }
 }
 
+// The 64 rounds of one block on its schedule words q (FIPS 180-4 section
+// 6.2.2 steps 2-4); the feed-forward only where `on` (the lane still has
+// blocks).
+__device__ __forceinline__ void rounds(uint32_t H[8], const uint4 q[16], bool on) {
+    uint32_t s[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s[i] = H[i];
+#pragma unroll
+    for (int g = 0; g < 16; ++g) {
+        const uint32_t w4[4] = {q[g].x, q[g].y, q[g].z, q[g].w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int t = 4 * g + k;
+            uint32_t& a = s[(8 - t) & 7];
+            uint32_t& bb = s[(9 - t) & 7];
+            uint32_t& c = s[(10 - t) & 7];
+            uint32_t& dd = s[(11 - t) & 7];
+            uint32_t& e = s[(12 - t) & 7];
+            uint32_t& f = s[(13 - t) & 7];
+            uint32_t& gg = s[(14 - t) & 7];
+            uint32_t& h = s[(15 - t) & 7];
+            const uint32_t t1 = h + kRound[t] + w4[k] + big_sigma1(e) + choose(e, f, gg);
+            const uint32_t t2 = big_sigma0(a) + majority(a, bb, c);
+            dd += t1;     // the new e
+            h = t1 + t2;  // the new a
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) H[i] = on ? H[i] + s[i] : H[i];
+}
+
+// The consumer's work for block b: pass the barrier of block b + 1 and issue
+// the reads of its words into `nxt`, then run block b's rounds on `cur`, so
+// the reads land under the rounds.
+__device__ __forceinline__ void consume(uint32_t b, uint32_t nmax, uint32_t nblk, uint32_t lane,
+                                        uint4 (*sched)[16][64], uint32_t H[8], const uint4 cur[16], uint4 nxt[16]) {
+    // `cur` has landed (read one block ago); waiting here, on every path and
+    // before the next reads, keeps the compiler from placing a wait for it
+    // where it would also wait for the reads issued below
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    if (b + 1 < nmax) {
+        lds_barrier();  // block b + 1's words are in buffer (b + 1) % 2
+#pragma unroll
+        for (int g = 0; g < 16; ++g) nxt[g] = sched[(b + 1) & 1][g][lane];
+    }
+    rounds(H, cur, b < nblk);
+}
+
 template <int kPairs>
 __global__ void __launch_bounds__(128 * kPairs) sha256_split_kernel(const LeafDesc* __restrict__ desc,
                                                                     uint64_t n_slots, uint64_t out_bound,
@@ -217,42 +265,17 @@ __global__ void __launch_bounds__(128 * kPairs) sha256_split_kernel(const LeafDe
     } else {
         uint32_t H[8];
         init_state(H);
-        for (uint32_t b = 0; b < nmax; ++b) {
-            lds_barrier();  // block b's words are in buffer b % 2
-            {
-                uint4(*buf)[64] = sched[pair][b & 1];
-                // all 64 words into registers first, one wait, then the rounds
-                // run without waiting on LDS
-                uint4 q[16];
+        // two register sets take turns: block b + 1's words are read into one
+        // while block b's rounds run on the other
+        uint4 A[16], B[16];
+        if (nmax > 0) {
+            lds_barrier();  // block 0's words are in buffer 0
 #pragma unroll
-                for (int g = 0; g < 16; ++g) q[g] = buf[g][lane];
-                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-                uint32_t s[8];
-#pragma unroll
-                for (int i = 0; i < 8; ++i) s[i] = H[i];
-#pragma unroll
-                for (int g = 0; g < 16; ++g) {
-                    const uint32_t w4[4] = {q[g].x, q[g].y, q[g].z, q[g].w};
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const int t = 4 * g + k;
-                        uint32_t& a = s[(8 - t) & 7];
-                        uint32_t& bb = s[(9 - t) & 7];
-                        uint32_t& c = s[(10 - t) & 7];
-                        uint32_t& dd = s[(11 - t) & 7];
-                        uint32_t& e = s[(12 - t) & 7];
-                        uint32_t& f = s[(13 - t) & 7];
-                        uint32_t& gg = s[(14 - t) & 7];
-                        uint32_t& h = s[(15 - t) & 7];
-                        const uint32_t t1 = h + kRound[t] + w4[k] + big_sigma1(e) + choose(e, f, gg);
-                        const uint32_t t2 = big_sigma0(a) + majority(a, bb, c);
-                        dd += t1;       // the new e
-                        h = t1 + t2;    // the new a
-                    }
-                }
-#pragma unroll
-                for (int i = 0; i < 8; ++i) H[i] = b < nblk ? H[i] + s[i] : H[i];
-            }
+            for (int g = 0; g < 16; ++g) A[g] = sched[pair][0][g][lane];
+        }
+        for (uint32_t b = 0; b < nmax; b += 2) {
+            consume(b, nmax, nblk, lane, sched[pair], H, A, B);
+            if (b + 1 < nmax) consume(b + 1, nmax, nblk, lane, sched[pair], H, B, A);
         }
         if (live && d.out < out_bound) store_digest(digests + 32 * d.out, H);
     }
