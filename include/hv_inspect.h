@@ -34,8 +34,8 @@ hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_b
  * one-wave kernel, 2 = always the two-wave kernel, 3 = always the two-wave
  * kernel with two producer/consumer pairs per workgroup (the layout it takes
  * above 64 leaves per compute unit).  Monitor scans (hv_monitor.h) take the
- * one-wave kernel under the automatic choice.  The digests do not depend on
- * it.  SHA-384 has one kernel.
+ * one-wave kernel under the automatic choice.  The same choice applies to
+ * SHA-384's two leaf kernels.  The digests do not depend on it.
  * Errors: HV_ERR_INVALID_ARG for another value. */
 hv_status hv_set_leaf_kernel(int choice);
 

@@ -226,7 +226,7 @@ hv_status hv_hash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, ui
     if (st != HV_OK || n_leaves == 0) return st;
 
     if ((st = leaf_timing_start(stream)) != HV_OK) return st;
-    const hipError_t e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.desc, n_leaves, n_leaves, leaf_digests, stream)
+    const hipError_t e = alg == HV_SHA384 ? hv::launch_sha384_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream)
                                           : hv::launch_sha256_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream);
     if (e != hipSuccess) return hip_fail(e, "leaf kernel");
     return leaf_timing_stop(stream);

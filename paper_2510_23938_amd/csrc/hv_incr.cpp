@@ -261,7 +261,7 @@ hv_status hv_rehash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, 
     if ((e = hv::launch_sched_select(L.msgs, L.off, n_msgs, chunk_bytes, R.list, n_listed, L.desc, stream)) !=
         hipSuccess)
         return hip_fail(e, "select kernel");
-    e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.desc, n_listed, n_leaves, leaf_digests, stream)
+    e = alg == HV_SHA384 ? hv::launch_sha384_auto(L.desc, n_listed, n_leaves, leaf_digests, stream)
                          : hv::launch_sha256_auto(L.desc, n_listed, n_leaves, leaf_digests, stream);
     if (e != hipSuccess) return hip_fail(e, "leaf kernel");
     return HV_OK;

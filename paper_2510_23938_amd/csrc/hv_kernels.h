@@ -69,6 +69,17 @@ hipError_t launch_monitor_compare(const uint8_t* digests, const uint8_t* ref, ui
 // unit of the current device (32768 on a 256-CU device).
 hipError_t launch_sha256_split(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                                bool two_pairs, hipStream_t s);
+// The two-wave SHA-384 leaf kernel (sha384_split.hip; same contract as
+// launch_sha384_leaves), one or two pairs per workgroup.
+hipError_t launch_sha384_split(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
+                               bool two_pairs, hipStream_t s);
+// SHA-384 leaf digests with the kernel the choice selects (the callers' entry),
+// by the same rules as launch_sha256_auto.
+hipError_t launch_sha384_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
+                              hipStream_t s, bool background = false);
+// Compute units of the current device (queried once per device; 0 if the
+// query fails, which makes the automatic choices take the one-wave kernels).
+uint32_t device_cus();
 // Leaf-kernel choice of the calling thread (hv_set_leaf_kernel): 0 automatic,
 // 1 one-wave kernel, 2 two-wave kernel, 3 two-wave kernel with two pairs per
 // workgroup.

@@ -122,7 +122,7 @@ hv_status hv_monitor_scan(const hv_monitor_plan* plan, uint64_t first_leaf, uint
                                           result, stream);
     if (e != hipSuccess) return hip_fail(e, "range kernel");
     if (n_slice == 0) return HV_OK;
-    e = plan->alg == HV_SHA384 ? hv::launch_sha384_leaves(S.desc, n_slice, n_slice, out, stream)
+    e = plan->alg == HV_SHA384 ? hv::launch_sha384_auto(S.desc, n_slice, n_slice, out, stream, true)
                                : hv::launch_sha256_auto(S.desc, n_slice, n_slice, out, stream, true);
     if (e != hipSuccess) return hip_fail(e, "leaf kernel");
     if ((e = hv::launch_monitor_compare(out, ref_digests, first_leaf, n_slice, D, result, stream)) != hipSuccess)

@@ -203,7 +203,7 @@ hv_status hv_plan_run(const hv_verify_plan* plan, uint8_t* leaf_digests, uint8_t
     if (plan->n_leaves > 0) {
         if ((st = leaf_timing_start(stream)) != HV_OK) return st;
         e = plan->alg == HV_SHA384
-                ? hv::launch_sha384_leaves(P.hash.desc, plan->n_leaves, plan->n_leaves, leaf_digests, stream)
+                ? hv::launch_sha384_auto(P.hash.desc, plan->n_leaves, plan->n_leaves, leaf_digests, stream)
                 : hv::launch_sha256_auto(P.hash.desc, plan->n_leaves, plan->n_leaves, leaf_digests, stream);
         if (e != hipSuccess) return hip_fail(e, "leaf kernel");
         if ((st = leaf_timing_stop(stream)) != HV_OK) return st;

@@ -199,7 +199,7 @@ hv_status hv_hash_host_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msg
                             hash_stream);
         if (st != HV_OK) break;
         uint8_t* out = leaf_digests + D * B.first_leaf;
-        e = alg == HV_SHA384 ? hv::launch_sha384_leaves(L.hash.desc, B.n_leaves, B.n_leaves, out, hash_stream)
+        e = alg == HV_SHA384 ? hv::launch_sha384_auto(L.hash.desc, B.n_leaves, B.n_leaves, out, hash_stream)
                              : hv::launch_sha256_auto(L.hash.desc, B.n_leaves, B.n_leaves, out, hash_stream);
         if (e != hipSuccess || (e = hipEventRecord(hashed[buf], hash_stream)) != hipSuccess)
             st = hip_fail(e, "leaf kernel");

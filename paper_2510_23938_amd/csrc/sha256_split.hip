@@ -27,6 +27,7 @@
 // (a select) and the digest store are per lane.
 #include "hv_kernels.h"
 #include "sha256_device.h"
+#include "split_common.h"
 
 #include <atomic>
 
@@ -47,12 +48,6 @@ constexpr int kMaxDevices = 64;
 __device__ __forceinline__ uint32_t block_valid(uint32_t nfull, uint32_t r, uint32_t b) {
     return b < nfull ? 64u : (b == nfull ? r : 0u);
 }
-
-// Global-memory pointers: loads through them are global (not flat) loads,
-// which the LDS counter does not track, so a wait for LDS leaves them in flight.
-typedef const __attribute__((address_space(1))) uint32_t* gwords;
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef const __attribute__((address_space(1))) u32x4* gquads;
 
 // Block b's bytes into D.  kAligned (the chunk starts on a 16-byte boundary):
 // the 16-byte granules that hold chunk bytes, with four 16-byte loads, into
@@ -76,14 +71,6 @@ __device__ __forceinline__ void load_block(uint64_t src, uint32_t valid, uint32_
 #pragma unroll
         for (int k = 0; k < 17; ++k) D[k] = (uint32_t)(4 * k) < sh + valid ? w[k] : 0u;
     }
-}
-
-// A workgroup barrier that orders LDS only: it waits for this wave's LDS
-// accesses, not for its global loads, so prefetches stay in flight across it.
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 // The 16 message words (big-endian) of block b from its dwords: a whole
@@ -125,7 +112,7 @@ __device__ __forceinline__ void produce(uint32_t b, uint64_t src, uint64_t total
     // `cur` has landed (its loads were issued one block ago); waiting here, on
     // every path and before the next loads, keeps the compiler from placing a
     // wait for them where it would also wait for the loads issued below
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    wait_vmem();
     if (b + 1 < nblk) load_block<kAligned>(src, block_valid(nfull, r, b + 1), b + 1, nxt);
     {  // every lane, also past its last block: see the kernel's comment on exec
         uint32_t W[16];
@@ -207,7 +194,7 @@ __device__ __forceinline__ void consume(uint32_t b, uint32_t nmax, uint32_t nblk
     // `cur` has landed (read one block ago); waiting here, on every path and
     // before the next reads, keeps the compiler from placing a wait for it
     // where it would also wait for the reads issued below
-    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    wait_lds();
     if (b + 1 < nmax) {
         lds_barrier();  // block b + 1's words are in buffer (b + 1) % 2
 #pragma unroll
@@ -281,6 +268,8 @@ __global__ void __launch_bounds__(128 * kPairs) sha256_split_kernel(const LeafDe
     }
 }
 
+}  // namespace
+
 // Compute units of the current device, queried once per device.
 uint32_t device_cus() {
     static std::atomic<int> cus[kMaxDevices];
@@ -293,8 +282,6 @@ uint32_t device_cus() {
     }
     return (uint32_t)n;
 }
-
-}  // namespace
 
 hipError_t launch_sha256_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                               hipStream_t s, bool background) {

@@ -465,8 +465,8 @@ def measure_hbm_read(nbytes=16 << 30, device="cuda", grid=None, reps=5) -> dict:
 
 
 def set_leaf_kernel(choice: str):
-    """SHA-256 leaf kernel for this thread: "auto", "one-wave", "two-wave" or "two-wave-compact" (two
-    producer/consumer pairs per workgroup); digests do not depend on it."""
+    """Leaf kernel (SHA-256 and SHA-384) for this thread: "auto", "one-wave", "two-wave" or
+    "two-wave-compact" (two producer/consumer pairs per workgroup); digests do not depend on it."""
     _check(lib.hv_set_leaf_kernel({"auto": 0, "one-wave": 1, "two-wave": 2, "two-wave-compact": 3}[choice]))
 
 

@@ -67,6 +67,61 @@ def test_mixed_batch(C):
     check_all(buf, host, ptrs, lens, starts, C, f"mixed C={C}")
 
 
+@pytest.fixture
+def leaf_kernel():
+    yield hv.set_leaf_kernel
+    hv.set_leaf_kernel("auto")
+
+
+@pytest.mark.parametrize("choice", ["one-wave", "two-wave", "two-wave-compact"])
+@pytest.mark.parametrize("align_off", [0, 5])
+@pytest.mark.parametrize("C", [128, 4096, 0])
+def test_leaf_kernels(C, align_off, choice, leaf_kernel):
+    # the one-wave kernel and the two-wave kernel (schedule on a producer wave;
+    # one or two pairs per workgroup) forced on the same inputs
+    leaf_kernel(choice)
+    lens = np.arange(0, 1301)
+    buf, host, ptrs, lens, starts = place(lens, align_off, seed=410 + align_off)
+    check_all(buf, host, ptrs, lens, starts, C, f"{choice} C={C} off={align_off}")
+
+
+def place_offsets(lens, offs, seed):
+    """Messages each at its own offset from a 16-byte boundary: (buf, host, ptrs, lens, starts)."""
+    starts = np.zeros(len(lens), dtype=np.uint64)
+    pos = 0
+    for i, n in enumerate(lens):
+        starts[i] = pos + int(offs[i])
+        pos += (int(n) + int(offs[i]) + 16 + 15) // 16 * 16
+    buf = W.random_bytes(max(pos, 1), seed, DEV)
+    host = buf.cpu().numpy()
+    ptrs = np.uint64(buf.data_ptr()) + starts
+    ptrs[lens == 0] = 0
+    return buf, host, ptrs, lens, starts
+
+
+@pytest.mark.parametrize("choice", ["auto", "two-wave", "two-wave-compact", "one-wave"])
+def test_mixed_alignment_and_two_pairs(choice, leaf_kernel):
+    # more than 64 chunks per CU (two pairs per workgroup under the two-wave
+    # kernel), random lengths, and 10% of the messages off 16-byte alignment
+    leaf_kernel(choice)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    n = 100 * cus
+    rng = np.random.default_rng(411)
+    lens = rng.integers(0, 1500, n).astype(np.uint64)
+    lens[rng.integers(0, n, 30)] = rng.integers(20000, 70000, 30).astype(np.uint64)
+    offs = rng.integers(0, 16, n) * (rng.random(n) < 0.1)
+    buf, host, ptrs, lens, starts = place_offsets(lens, offs, 412)
+    check_all(buf, host, ptrs, lens, starts, 0, f"{choice} n={n}")
+
+
+@pytest.mark.parametrize("choice", ["one-wave", "two-wave"])
+def test_long_chunks(choice, leaf_kernel):
+    leaf_kernel(choice)
+    lens = [(4 << 20) + 111, (4 << 20) + 112, 3 << 20, 1, 0]
+    buf, host, ptrs, lens, starts = place(lens, 0, seed=413)
+    check_all(buf, host, ptrs, lens, starts, 0, f"{choice} long")
+
+
 def test_empty_cases():
     v = hv.Verifier(DEV, ALG)
     leaves, seg = v.leaf_digests((np.zeros(0, np.uint64), np.zeros(0, np.uint64)), 128)
