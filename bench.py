@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -97,6 +98,29 @@ def traffic_for_current_kernel(alg="sha256", config=5):
     return rec.get("hbm_bytes_per_launch")
 
 
+def host_cpu_info():
+    """The host CPU as lscpu reports it (model, sockets, cores, SMT), else /proc/cpuinfo's model name."""
+    info = {"host_cpu": "", "host_cpus_visible": os.cpu_count()}
+    fields = {"Model name": "host_cpu", "Socket(s)": "host_sockets", "Core(s) per socket": "host_cores_per_socket",
+              "Thread(s) per core": "host_threads_per_core"}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10, check=True).stdout
+        for ln in out.splitlines():
+            key, _, val = ln.partition(":")
+            if key.strip() in fields:
+                val = val.strip()
+                info[fields[key.strip()]] = int(val) if val.isdigit() else val
+    except (OSError, subprocess.SubprocessError):
+        pass
+    if not info["host_cpu"]:
+        try:
+            with open("/proc/cpuinfo") as f:
+                info["host_cpu"] = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+        except OSError:
+            pass
+    return info
+
+
 def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
     """The oracle (plain C, threaded over chunks) on the first whole chunks of
     the first messages, about sample_bytes in all, one message at a time so
@@ -139,15 +163,9 @@ def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
     oracle.leaf_digests_mt([host], C, 1, alg)
     per_core = host.size / (time.perf_counter() - t0) / 1e9
     del host
-    model = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
-    except OSError:
-        pass
     return {
         "value": round(nbytes / dt / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-        "single_thread_GBps": round(per_core, 4), "host_cpu": model, "host_cpus_visible": os.cpu_count(),
+        "single_thread_GBps": round(per_core, 4), **host_cpu_info(),
         "sample": f"first {nbytes} bytes ({n_leaves} whole chunks of {n_msgs} message(s)) of this workload, one "
                   f"message at a time; oracle chunk digests on {threads} threads + the Merkle root over them; "
                   f"device-to-host copies not timed",
