@@ -221,7 +221,11 @@ def _ptr_len(msgs):
 
 
 def hv_leaf_layout(ptrs, lens, chunk_bytes: int):
-    arr = _msg_array(ptrs, lens)
+    return _layout_of(_msg_array(ptrs, lens), chunk_bytes)
+
+
+def _layout_of(arr: np.ndarray, chunk_bytes: int):
+    """(seg_offsets, n_leaves) of an hv_msg array as _msg_array builds it."""
     n = len(arr)
     seg = np.zeros(n + 1, dtype=np.uint64)
     n_leaves = ctypes.c_uint64(0)
@@ -257,8 +261,8 @@ def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace |
     ``ptrs``/``lens``): ([n_leaves, D] uint8 device tensor, seg_offsets), D the digest size."""
     _, D = _alg(alg)
     ptrs, lens = _ptr_len(msgs)
-    seg, n_leaves = hv_leaf_layout(ptrs, lens, chunk_bytes)
     arr = _msg_array(ptrs, lens)
+    seg, n_leaves = _layout_of(arr, chunk_bytes)
     n = len(arr)
     dev = torch.device(device)
     if out is None:
@@ -292,8 +296,8 @@ def hv_hash_host_chunks(host_msgs, chunk_bytes: int, batch_bytes: int = 1 << 30,
     code, D = _alg(alg)
     ptrs, lens = host_messages_of(host_msgs) if not (isinstance(host_msgs, tuple) and len(host_msgs) == 2
                                                      and isinstance(host_msgs[0], np.ndarray)) else host_msgs
-    seg, n_leaves = hv_leaf_layout(ptrs, lens, chunk_bytes)
     arr = _msg_array(ptrs, lens)
+    seg, n_leaves = _layout_of(arr, chunk_bytes)
     n = len(arr)
     dev = torch.device(device)
     need = lib.hv_stream_workspace_bytes(arr.ctypes.data if n else None, n, chunk_bytes, batch_bytes)
@@ -362,8 +366,8 @@ def hv_leaf_schedule(msgs, chunk_bytes: int, device="cuda") -> np.ndarray:
     """The scheduler's leaf table, in schedule order: uint64 [n_leaves, 3] of
     (source address, byte length, leaf index).  For tests of the scheduler."""
     ptrs, lens = _ptr_len(msgs)
-    _, n_leaves = hv_leaf_layout(ptrs, lens, chunk_bytes)
     arr = _msg_array(ptrs, lens)
+    _, n_leaves = _layout_of(arr, chunk_bytes)
     n = len(arr)
     table = np.zeros((n_leaves, 3), dtype=np.uint64)
     dev = torch.device(device)
@@ -537,7 +541,7 @@ class Pipeline:
         self.keepalive = msgs
         arr = _msg_array(ptrs, lens)
         self.n_msgs = len(arr)
-        self.seg, self.n_leaves = hv_leaf_layout(ptrs, lens, self.C)
+        self.seg, self.n_leaves = _layout_of(arr, self.C)
         self.total_bytes = int(np.asarray(lens, dtype=np.uint64).sum()) if self.n_msgs else 0
         manifest = 1 if mode == "manifest" else 0
         nbytes = lib.hv_plan_bytes(code, arr.ctypes.data if self.n_msgs else None, self.n_msgs, self.C, manifest)
