@@ -501,6 +501,8 @@ class Verifier:
     def roots(self, msgs, chunk_bytes: int):
         """(per-message roots [n, D], leaf digests, seg_offsets)."""
         leaves, seg = self.leaf_digests(msgs, chunk_bytes)
+        if len(seg) == 1:  # no messages, no roots (hv_merkle_reduce takes at least one segment)
+            return torch.empty((0, self.D), dtype=torch.uint8, device=self.device), leaves, seg
         return hv_merkle_reduce(leaves, seg, self.ws_tree, alg=self.alg), leaves, seg
 
     def manifest_root(self, msgs, chunk_bytes: int) -> torch.Tensor:

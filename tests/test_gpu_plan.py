@@ -65,6 +65,12 @@ def test_empty_sets(alg):
     pipe = hv.Pipeline((np.zeros(3, np.uint64), np.zeros(3, np.uint64)), 128, "manifest", DEV, alg=alg)
     assert pipe.n_leaves == 0
     assert bytes(pipe.compute().cpu().numpy().reshape(-1)) == oracle.mth([e, e, e], alg)
+    # the one-shot calls agree: no messages is the tree over no roots
+    v = hv.Verifier(DEV, alg)
+    none = (np.zeros(0, np.uint64), np.zeros(0, np.uint64))
+    assert bytes(v.manifest_root(none, 128).cpu().numpy().reshape(-1)) == e
+    assert bytes(v.single_tree_root(none, 128).cpu().numpy().reshape(-1)) == e
+    assert hv.manifest_root({}, 128, alg=alg) == e
 
 
 @pytest.mark.parametrize("alg", ["sha256", "sha384"])

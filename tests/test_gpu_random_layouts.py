@@ -1,0 +1,100 @@
+"""Seeded random layouts through the whole path against the CPU oracle.
+
+Each case draws a message count, lengths (clustered around block boundaries,
+with empty and multi-block messages), a placement offset 0..15 per message, a
+chunk size, the hash, the leaf-kernel choice and the root form (one tree or
+per-message trees plus a manifest), then checks every leaf digest, every
+segment root and the top root bit for bit.  The cases are small, so together
+they cross the scheduler's buckets, both leaf kernels (one or two producer /
+consumer pairs per workgroup), both load paths and the Merkle tiles' ragged
+edges far more often than the fixed tests do.  Expected values come only from
+``oracle``.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import oracle
+
+hv = pytest.importorskip("paper_2510_23938_amd.hv")
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda")
+CASES = 48
+CHOICES = ["auto", "one-wave", "two-wave", "two-wave-compact"]
+
+
+def threads():
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def draw(rng, alg):
+    B = 64 if alg == "sha256" else 128
+    n = int(rng.choice([0, 1, 2, 7, 64, 65, 129, int(rng.integers(1, 300))]))
+    kind = rng.integers(0, 4, n)
+    lens = np.where(kind == 0, rng.integers(0, 3 * B, n),                          # short, around one block
+            np.where(kind == 1, rng.integers(1, 40, n) * B + rng.integers(-2, 3, n),  # near block multiples
+            np.where(kind == 2, rng.integers(0, 200_000, n), 0)))                   # long, or empty
+    lens = np.maximum(lens, 0).astype(np.uint64)
+    offs = rng.integers(0, 16, n) * (rng.random(n) < 0.5)
+    C = int(rng.choice([0, B, 3 * B, 4096, 65536]))
+    return lens, offs, C
+
+
+def place(lens, offs, seed):
+    starts = np.zeros(len(lens), dtype=np.uint64)
+    pos = 0
+    for i, L in enumerate(lens):
+        starts[i] = pos + int(offs[i])
+        pos += (int(L) + int(offs[i]) + 16 + 15) // 16 * 16
+    buf = W.random_bytes(max(pos, 1), seed, DEV)
+    host = buf.cpu().numpy()
+    ptrs = np.uint64(buf.data_ptr()) + starts
+    ptrs[lens == 0] = 0
+    return buf, host, ptrs, starts
+
+
+@pytest.fixture
+def leaf_kernel():
+    yield hv.set_leaf_kernel
+    hv.set_leaf_kernel("auto")
+
+
+@pytest.mark.parametrize("case", range(CASES))
+def test_random_layout(case, leaf_kernel):
+    rng = np.random.default_rng(20251023 + case)
+    alg = "sha256" if case % 2 == 0 else "sha384"
+    choice = CHOICES[(case // 2) % len(CHOICES)]
+    manifest = (case // 8) % 2 == 1
+    lens, offs, C = draw(rng, alg)
+    tag = f"case {case}: {alg}, {choice}, {'manifest' if manifest else 'one tree'}, {len(lens)} messages, C={C}"
+    leaf_kernel(choice)
+    buf, host, ptrs, starts = place(lens, offs, 600 + case)
+    v = hv.Verifier(DEV, alg)
+    leaves, seg = v.leaf_digests((ptrs, lens), C)
+    if manifest:
+        roots, _, _ = v.roots((ptrs, lens), C)
+        top = v.manifest_root((ptrs, lens), C)
+    else:
+        top = hv.hv_merkle_reduce(leaves, np.array([0, leaves.shape[0]], dtype=np.uint64), v.ws_tree, alg=alg)
+    torch.cuda.synchronize()
+
+    msgs = [host[int(s):int(s) + int(L)] for s, L in zip(starts, lens)]
+    want = oracle.leaf_digests_mt(msgs, C, threads(), alg)
+    got = leaves.cpu().numpy()
+    if not np.array_equal(got, want):
+        bad = np.nonzero((got != want).any(axis=1))[0]
+        m = int(np.searchsorted(seg, bad[0], side="right") - 1)
+        raise AssertionError(f"{tag}: {len(bad)} leaf digests differ, first leaf {bad[0]} "
+                             f"(message {m}, length {int(lens[m])}, offset {int(offs[m])})")
+    if manifest:
+        want_roots = oracle.seg_roots_from_leaves(want, np.diff(seg), alg)
+        assert [bytes(r) for r in roots.cpu().numpy()] == want_roots, f"{tag}: segment roots differ"
+        want_top = oracle.mth(want_roots, alg)
+    else:
+        want_top = oracle.mth([bytes(d) for d in want], alg)
+    assert bytes(top.cpu().numpy().reshape(-1)) == want_top, f"{tag}: top root differs"
+    assert v.verify_root(top, want_top), f"{tag}: verify rejects the right root"
