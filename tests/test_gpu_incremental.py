@@ -111,3 +111,24 @@ def test_update_after_partial_change_sha384(C):
     assert torch.equal(roots, full_roots)
     host = [b.cpu().numpy() for b in bufs]
     assert [bytes(r) for r in roots.cpu().numpy()] == [oracle.seg_root_alg(h, C, alg) for h in host]
+
+
+def test_empty_segments_and_empty_lists():
+    # segments without leaves keep the empty-tree root; an update with no
+    # listed leaves and a rehash of no leaves change nothing
+    e = oracle.mth([])
+    seg = np.array([0, 0, 0], dtype=np.uint64)
+    none = torch.empty((0, 32), dtype=torch.uint8, device=DEV)
+    tree = hv.Tree(none, seg)
+    torch.cuda.synchronize()
+    assert [bytes(r) for r in tree.roots.cpu().numpy()] == [e, e]
+    roots = tree.update(none, np.zeros(0, dtype=np.uint64))
+    torch.cuda.synchronize()
+    assert [bytes(r) for r in roots.cpu().numpy()] == [e, e]
+
+    msgs = [W.random_bytes(5000, 470 + i, DEV) for i in range(2)]
+    leaves, seg = hv.hv_hash_chunks(msgs, 4096)
+    before = leaves.clone()
+    hv.hv_rehash_chunks(msgs, 4096, np.zeros(0, dtype=np.uint64), leaves)
+    torch.cuda.synchronize()
+    assert torch.equal(leaves, before)

@@ -126,3 +126,17 @@ def test_verify_model_one_call(alg, C, mode):
     assert r["root"] == want and not r["integrity_verified"]
     r = hv.verify_model((ptrs, lens), C, None, alg=alg, mode=mode)
     assert r["root"] == want and not r["integrity_verified"]
+
+
+@pytest.mark.parametrize("alg", ["sha256", "sha384"])
+def test_verify_model_empty_set(alg):
+    # no messages: the root is the empty tree's in both forms, and a wrong
+    # expected root is a False verdict, not an error
+    e = oracle.mth([], alg)
+    none = (np.zeros(0, np.uint64), np.zeros(0, np.uint64))
+    for mode in ("manifest", "single"):
+        r = hv.verify_model(none, 128, e, alg=alg, mode=mode)
+        assert r["integrity_verified"] and r["root"] == e
+        bad = bytearray(e)
+        bad[0] ^= 1
+        assert not hv.verify_model(none, 128, bytes(bad), alg=alg, mode=mode)["integrity_verified"]

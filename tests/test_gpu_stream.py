@@ -85,3 +85,18 @@ def test_streamed_sha384_equal_resident_and_oracle(C, batch):
     assert torch.equal(got, resident)
     want = oracle.leaf_digests_mt([m.numpy() for m in msgs], C, 8, "sha384")
     assert np.array_equal(got.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("C", [4096, 0])
+def test_stream_empty_sets(C):
+    # no messages, and messages that are all empty: the same digests as the
+    # resident path (none with C > 0; one SHA-256("") per message with C = 0)
+    got, seg = hv.hv_hash_host_chunks((np.zeros(0, np.uint64), np.zeros(0, np.uint64)), C, 1 << 20)
+    torch.cuda.synchronize()
+    assert got.shape == (0, 32) and list(seg) == [0]
+    msgs = [torch.empty(0, dtype=torch.uint8) for _ in range(3)]
+    got, seg = hv.hv_hash_host_chunks(msgs, C, 1 << 20)
+    resident, seg2 = hv.hv_hash_chunks([m.to(DEV) for m in msgs], C)
+    torch.cuda.synchronize()
+    assert np.array_equal(seg, seg2) and torch.equal(got, resident)
+    assert [bytes(d) for d in got.cpu().numpy()] == ([oracle.digest(b"")] * 3 if C == 0 else [])
