@@ -26,6 +26,11 @@
  *     caller-provided workspace of the size the *_workspace_bytes call gives.
  *   - Calls are asynchronous on `stream` unless marked "synchronous".  Input
  *     bytes must stay valid and unmodified until the stream work completes.
+ *     Host arrays a call takes (message tables, offset, leaf and dirty lists,
+ *     expected roots) are an exception: they are read, and uploaded where the
+ *     device needs them, before the call returns, whatever memory they are in
+ *     (pageable or pinned); such a call returns once `stream` has reached and
+ *     finished its uploads.
  *   - All argument checks happen before any work is queued; on a non-OK
  *     status nothing was launched (except HV_ERR_HIP, which reports a failed
  *     launch or copy) and hv_last_error() describes the problem.
@@ -123,8 +128,7 @@ size_t hv_merkle_workspace_bytes(uint64_t n_nodes, uint32_t n_seg);
  *   roots:       device, n_seg * 32 bytes, 16-byte aligned, written.
  *   workspace:   device, >= hv_merkle_workspace_bytes(seg_offsets[n_seg], n_seg).
  * The host plans ceil(depth / 9) launches from seg_offsets and uploads that
- * plan (a copy from pageable memory, so the call returns once the stream has
- * reached it).
+ * plan before returning (so the call returns once the stream has reached it).
  * Errors: HV_ERR_INVALID_ARG for n_seg == 0, NULL or misaligned pointers,
  * offsets that do not start at 0 or decrease; HV_ERR_WORKSPACE; HV_ERR_HIP. */
 hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg,

@@ -47,8 +47,8 @@ typedef struct {
 /* Device bytes hv_monitor_init needs for n_msgs messages. */
 size_t hv_monitor_plan_bytes(uint32_t n_msgs);
 
-/* Build a plan: uploads the message table (pageable, so this returns once
- * the stream has reached the upload) and queues the per-message leaf
+/* Build a plan: uploads the message table before returning (so this returns
+ * once the stream has reached the upload) and queues the per-message leaf
  * offsets on `stream`.
  *   msgs: host, n_msgs entries (device addresses, as hv_hash_chunks_alg).
  *   plan_memory: device, >= hv_monitor_plan_bytes(n_msgs), 256-byte aligned.

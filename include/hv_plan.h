@@ -44,7 +44,7 @@ typedef struct {
  * arguments hv_plan_init would reject. */
 size_t hv_plan_bytes(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, int manifest);
 
-/* Build a plan.  Uploads from pageable host memory (so it returns once the
+/* Build a plan.  Uploads the host tables before returning (so it returns once the
  * stream has reached them) and queues the scheduling kernels on `stream`.
  *   msgs: host, n_msgs entries (device addresses), as hv_hash_chunks_alg.
  *   plan_memory: device, >= hv_plan_bytes(...), 256-byte aligned.

@@ -192,7 +192,7 @@ hv_status schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, bo
 
     const HashLayout& L = *L_out;
     static_assert(sizeof(hv_msg) == sizeof(hv::MsgDesc), "hv_msg layout");
-    hipError_t e = hipMemcpyAsync(L.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
+    hipError_t e = hipMemcpyWithStream(L.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "descriptor upload");
     return hvh::queue_schedule(L.msgs, n_msgs, chunk_bytes, n_full, n_leaves, L, stream);
 }
@@ -295,8 +295,8 @@ hv_status hv_merkle_reduce_alg(hv_alg alg, const uint8_t* nodes, const uint64_t*
     if (st != HV_OK) return st;
 
     const MerkleLayout L = merkle_layout(workspace, n_nodes, n_seg, D);
-    hipError_t e = hipMemcpyAsync(L.table, table.data(), table.size() * sizeof(uint64_t), hipMemcpyHostToDevice,
-                                  stream);
+    hipError_t e = hipMemcpyWithStream(L.table, table.data(), table.size() * sizeof(uint64_t), hipMemcpyHostToDevice,
+                                       stream);
     if (e != hipSuccess) return hip_fail(e, "plan upload");
     const uint8_t* in = nodes;
     for (int k = 1; k <= launches; ++k) {

@@ -149,7 +149,8 @@ hv_status hv_tree_build_alg(hv_alg alg, const uint8_t* leaf_digests, const uint6
     if ((uintptr_t)tree % kAlign != 0) return fail(HV_ERR_WORKSPACE, "tree is not 256-byte aligned");
     const TreeLayout T = tree_layout(tree, rows, n_seg, levels, D);
     const size_t w = (size_t)n_seg + 1;
-    hipError_t e = hipMemcpyAsync(T.table, rows.data(), rows.size() * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
+    hipError_t e =
+        hipMemcpyWithStream(T.table, rows.data(), rows.size() * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "table upload");
     if ((e = hv::launch_tree_leaf_level(ka, leaf_digests, n, T.level[0], stream)) != hipSuccess)
         return hip_fail(e, "leaf level");
@@ -197,11 +198,12 @@ hv_status hv_tree_update_alg(hv_alg alg, const uint8_t* leaf_digests, const uint
     const TreeLayout T = tree_layout(tree, rows, n_seg, levels, D);
     const size_t w = (size_t)n_seg + 1;
     // the offset table is re-sent so the kernels walk exactly the layout planned here
-    hipError_t e = hipMemcpyAsync(T.table, rows.data(), rows.size() * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
+    hipError_t e =
+        hipMemcpyWithStream(T.table, rows.data(), rows.size() * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "table upload");
     if (n_dirty > 0) {
         const UpdateLayout U = update_layout(workspace, n_dirty);
-        if ((e = hipMemcpyAsync(U.dirty, dirty, n_dirty * sizeof(uint64_t), hipMemcpyHostToDevice, stream)) !=
+        if ((e = hipMemcpyWithStream(U.dirty, dirty, n_dirty * sizeof(uint64_t), hipMemcpyHostToDevice, stream)) !=
             hipSuccess)
             return hip_fail(e, "dirty list upload");
         if ((e = hv::launch_tree_locate(U.dirty, n_dirty, T.table, n_seg, U.seg_of, U.local, stream)) != hipSuccess)
@@ -250,9 +252,9 @@ hv_status hv_rehash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, 
     if (n_listed == 0) return HV_OK;
     const RehashLayout R = rehash_layout(workspace, n_msgs, n_listed);
     const HashLayout& L = R.hash;
-    hipError_t e = hipMemcpyAsync(L.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
+    hipError_t e = hipMemcpyWithStream(L.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
     if (e == hipSuccess)
-        e = hipMemcpyAsync(R.list, leaves, n_listed * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
+        e = hipMemcpyWithStream(R.list, leaves, n_listed * sizeof(uint64_t), hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "upload");
     if ((e = hv::launch_sched_count(L.msgs, n_msgs, chunk_bytes, L.cnt, stream)) != hipSuccess)
         return hip_fail(e, "count kernel");

@@ -150,11 +150,12 @@ hv_status hv_plan_init(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t
     hipError_t e;
     static_assert(sizeof(hv_msg) == sizeof(hv::MsgDesc), "hv_msg layout");
     if (n_msgs > 0 &&
-        (e = hipMemcpyAsync(P.hash.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream)) != hipSuccess)
+        (e = hipMemcpyWithStream(P.hash.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream)) !=
+            hipSuccess)
         return hip_fail(e, "message table upload");
     for (int i = 0; i < 2; ++i)
-        if (p.rows[i] > 0 && (e = hipMemcpyAsync(P.table[i], p.table[i].data(), p.rows[i] * sizeof(uint64_t),
-                                                 hipMemcpyHostToDevice, stream)) != hipSuccess)
+        if (p.rows[i] > 0 && (e = hipMemcpyWithStream(P.table[i], p.table[i].data(), p.rows[i] * sizeof(uint64_t),
+                                                      hipMemcpyHostToDevice, stream)) != hipSuccess)
             return hip_fail(e, "merkle table upload");
     if (n_msgs > 0 &&
         (st = queue_schedule(P.hash.msgs, n_msgs, chunk_bytes, p.n_full, p.n_leaves, P.hash, stream)) != HV_OK)

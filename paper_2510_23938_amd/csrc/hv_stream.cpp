@@ -161,8 +161,8 @@ hv_status hv_hash_host_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msg
     for (size_t b = 0; b < P.batches.size(); ++b)
         for (size_t i = P.batches[b].p0; i < P.batches[b].p1; ++i)
             descs[i] = {(uint64_t)(uintptr_t)(L.stage[b % 2] + P.pieces[i].stage_off), P.pieces[i].len};
-    hipError_t e = hipMemcpyAsync(L.descs, descs.data(), descs.size() * sizeof(hv::MsgDesc), hipMemcpyHostToDevice,
-                                  hash_stream);
+    hipError_t e = hipMemcpyWithStream(L.descs, descs.data(), descs.size() * sizeof(hv::MsgDesc),
+                                       hipMemcpyHostToDevice, hash_stream);
     if (e != hipSuccess) return hip_fail(e, "descriptor upload");
 
     hipEvent_t copied[2] = {nullptr, nullptr}, hashed[2] = {nullptr, nullptr};

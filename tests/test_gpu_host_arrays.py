@@ -1,0 +1,83 @@
+"""Host arrays a call takes are read before it returns, also from pinned memory.
+
+A pinned message table points at buffers A; right after each call returns,
+the table is rewritten to point at buffers B of the same lengths (so any
+reading of it stays in bounds).  The stream is kept busy before each call,
+so an upload still waiting in the stream would read the rewritten table and
+hash B.  The digests must be A's, from the oracle.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import oracle
+
+hv = pytest.importorskip("paper_2510_23938_amd.hv")
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda")
+C = 4096
+LENS = [5000, 70000, 1, 4096, 0, 12289]
+
+
+@pytest.fixture
+def buffers():
+    A = [W.random_bytes(L, 1300 + i, DEV) for i, L in enumerate(LENS)]
+    B = [W.random_bytes(L, 1400 + i, DEV) for i, L in enumerate(LENS)]
+    torch.cuda.synchronize()
+    pinned = torch.empty((len(LENS), 2), dtype=torch.int64, pin_memory=True)
+    table = pinned.numpy().view(np.uint64)
+
+    def point(bufs):
+        table[:, 0] = [b.data_ptr() if b.numel() else 0 for b in bufs]
+        table[:, 1] = LENS
+
+    want = oracle.leaf_digests_mt([a.cpu().numpy() for a in A], C, 4)
+    yield A, B, table, point, want
+    torch.cuda.synchronize()
+
+
+def busy():
+    torch.cuda._sleep(20_000_000)  # about 10 ms of queued work ahead of the call
+
+
+def test_hash_chunks_reads_a_pinned_table_during_the_call(buffers):
+    A, B, table, point, want = buffers
+    n = len(LENS)
+    point(A)
+    seg, n_leaves = hv.hv_leaf_layout(table[:, 0].copy(), table[:, 1].copy(), C)
+    out = torch.empty((n_leaves, 32), dtype=torch.uint8, device=DEV)
+    ws = hv.Workspace(DEV).get(hv.lib.hv_hash_workspace_bytes(n, n_leaves))
+    busy()
+    st = hv.lib.hv_hash_chunks(table.ctypes.data, n, C, out.data_ptr(), ws.data_ptr(), ws.numel(), hv._stream(DEV))
+    point(B)
+    torch.cuda.synchronize()
+    assert st == hv.HV_OK
+    assert np.array_equal(out.cpu().numpy(), want)
+
+
+def test_plan_init_reads_a_pinned_table_during_the_call(buffers):
+    A, B, table, point, want = buffers
+    n = len(LENS)
+    point(A)
+    nbytes = hv.lib.hv_plan_bytes(hv.HV_SHA256, table.ctypes.data, n, C, 1)
+    mem = hv.Workspace(DEV).get(nbytes)
+    plan = hv.hv_verify_plan()
+    busy()
+    st = hv.lib.hv_plan_init(hv.HV_SHA256, table.ctypes.data, n, C, 1, mem.data_ptr(), mem.numel(),
+                             ctypes.byref(plan), hv._stream(DEV))
+    point(B)
+    assert st == hv.HV_OK
+    leaves = torch.empty((int(plan.n_leaves), 32), dtype=torch.uint8, device=DEV)
+    roots = torch.empty((n, 32), dtype=torch.uint8, device=DEV)
+    root = torch.empty((1, 32), dtype=torch.uint8, device=DEV)
+    st = hv.lib.hv_plan_run(ctypes.byref(plan), leaves.data_ptr(), roots.data_ptr(), root.data_ptr(), None, None,
+                            hv._stream(DEV))
+    torch.cuda.synchronize()
+    assert st == hv.HV_OK
+    assert np.array_equal(leaves.cpu().numpy(), want)
+    counts = [oracle.chunk_count(L, C) for L in LENS]
+    assert bytes(root.cpu().numpy().reshape(-1)) == oracle.mth(oracle.seg_roots_from_leaves(want, counts))
