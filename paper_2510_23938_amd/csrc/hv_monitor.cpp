@@ -74,7 +74,8 @@ hv_status hv_monitor_init(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint6
     hipError_t e;
     if (n_msgs > 0) {
         static_assert(sizeof(hv_msg) == sizeof(hv::MsgDesc), "hv_msg layout");
-        if ((e = hipMemcpyWithStream(P.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream)) != hipSuccess)
+        if ((e = hipMemcpyWithStream(P.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream)) !=
+            hipSuccess)
             return hip_fail(e, "message table upload");
         if ((e = hv::launch_sched_count(P.msgs, n_msgs, chunk_bytes, P.cnt, stream)) != hipSuccess)
             return hip_fail(e, "count kernel");
