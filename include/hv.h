@@ -72,7 +72,8 @@ enum { HV_DIGEST_BYTES = 32 };
  * kernel listings and the 48-byte digest of its C ABI (Implementation).  With
  * SHA-384 every digest, Merkle node and root is 48 bytes, the tree is RFC 6962
  * with SHA-384 as its hash, and chunk_bytes must be 0 or a multiple of 128. */
-typedef enum { HV_SHA256 = 0, HV_SHA384 = 1 } hv_alg;
+typedef int32_t hv_alg; /* an int, not an enum: any value a caller passes is well defined, and rejected if unknown */
+enum { HV_SHA256 = 0, HV_SHA384 = 1 };
 
 /* Leaf layout (synchronous, host only, touches no device memory).
  * Chunking (Algorithm 1): a message of L bytes with chunk size C > 0 has
