@@ -39,6 +39,13 @@ hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_b
  * Errors: HV_ERR_INVALID_ARG for another value. */
 hv_status hv_set_leaf_kernel(int choice);
 
+/* The leaf kernel a hash call over n_leaves leaves would run on the current
+ * device under this thread's choice: *kernel = 1 (one-wave), 2 (two-wave, one
+ * producer/consumer pair per workgroup) or 3 (two-wave, two pairs).  Monitor
+ * scans take the one-wave kernel under the automatic choice.
+ * Errors: HV_ERR_INVALID_ARG for a NULL kernel. */
+hv_status hv_leaf_kernel_for(uint64_t n_leaves, int* kernel);
+
 #ifdef __cplusplus
 }
 #endif

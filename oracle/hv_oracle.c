@@ -374,6 +374,7 @@ typedef struct {
     uint8_t* out;
     uint64_t n_leaves;
     uint64_t next;                /* next leaf to take (guarded by lock) */
+    uint64_t grab;                /* leaves a thread takes at a time */
     pthread_mutex_t lock;
 } mt_job;
 
@@ -383,7 +384,7 @@ static void* mt_worker(void* arg) {
     for (;;) {
         pthread_mutex_lock(&j->lock);
         uint64_t leaf = j->next;
-        uint64_t take = 64;       /* leaves per grab */
+        uint64_t take = j->grab;
         if (leaf + take > j->n_leaves) take = j->n_leaves - leaf;
         j->next = leaf + take;
         pthread_mutex_unlock(&j->lock);
@@ -424,8 +425,13 @@ uint64_t oracle_leaf_digests_alg_mt(int alg, const uint8_t* const* msgs, const u
     j.alg = alg;
     j.msgs = msgs; j.lens = lens; j.first_leaf = first; j.n_msgs = n_msgs; j.C = C;
     j.out = out; j.n_leaves = total; j.next = 0;
-    pthread_mutex_init(&j.lock, NULL);
     if (nthreads < 1) nthreads = 1;
+    /* about eight grabs per thread, 1..64 leaves each, so that few large
+     * chunks still spread over every thread */
+    j.grab = total / ((uint64_t)nthreads * 8);
+    if (j.grab < 1) j.grab = 1;
+    if (j.grab > 64) j.grab = 64;
+    pthread_mutex_init(&j.lock, NULL);
     pthread_t* th = (pthread_t*)malloc(sizeof(pthread_t) * (size_t)nthreads);
     /* Workers drain the shared counter, so the result is complete even if
      * fewer threads than asked for could be started. */

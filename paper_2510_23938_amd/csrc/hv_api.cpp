@@ -394,6 +394,12 @@ hv_status hv_set_leaf_kernel(int choice) {
     return HV_OK;
 }
 
+hv_status hv_leaf_kernel_for(uint64_t n_leaves, int* kernel) {
+    if (kernel == nullptr) return fail(HV_ERR_INVALID_ARG, "kernel is NULL");
+    *kernel = hv::leaf_kernel_for(n_leaves, false);
+    return HV_OK;
+}
+
 hv_status hv_set_kernel_timing(int enable) {
     g_timing.enabled = enable != 0;
     return HV_OK;

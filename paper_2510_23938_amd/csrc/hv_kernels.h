@@ -77,6 +77,10 @@ hipError_t launch_sha384_split(const LeafDesc* desc, uint64_t n_slots, uint64_t 
 // by the same rules as launch_sha256_auto.
 hipError_t launch_sha384_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                               hipStream_t s, bool background = false);
+// The leaf kernel a call over n_slots leaves takes under this thread's choice
+// on the current device: 1 one-wave, 2 two-wave with one pair per workgroup,
+// 3 two-wave with two pairs (both hashes use this rule).
+int leaf_kernel_for(uint64_t n_slots, bool background);
 // Compute units of the current device (queried once per device; 0 if the
 // query fails, which makes the automatic choices take the one-wave kernels).
 uint32_t device_cus();

@@ -283,8 +283,7 @@ uint32_t device_cus() {
     return (uint32_t)n;
 }
 
-hipError_t launch_sha256_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
-                              hipStream_t s, bool background) {
+int leaf_kernel_for(uint64_t n_slots, bool background) {
     const int choice = leaf_kernel_choice();
     const uint64_t cus = device_cus();
     // the two-wave kernel while every CU holds one workgroup at most (two
@@ -292,10 +291,15 @@ hipError_t launch_sha256_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t o
     // each run two waves and the one-wave kernel is faster.  Background work
     // keeps the one-wave kernel: the two-wave kernel spends two waves per 64
     // chunks to shorten each chain, about 1.3x the CU time per byte.
-    if (choice == 1 || (choice == 0 && (background || n_slots > 64 * kMaxPairs * cus)))
-        return launch_sha256_leaves(desc, n_slots, out_bound, digests, s);
-    const bool two_pairs = choice == 3 || n_slots > 64 * cus;
-    return launch_sha256_split(desc, n_slots, out_bound, digests, two_pairs, s);
+    if (choice == 1 || (choice == 0 && (background || n_slots > 64 * kMaxPairs * cus))) return 1;
+    return choice == 3 || n_slots > 64 * cus ? 3 : 2;
+}
+
+hipError_t launch_sha256_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
+                              hipStream_t s, bool background) {
+    const int k = leaf_kernel_for(n_slots, background);
+    if (k == 1) return launch_sha256_leaves(desc, n_slots, out_bound, digests, s);
+    return launch_sha256_split(desc, n_slots, out_bound, digests, k == 3, s);
 }
 
 hipError_t launch_sha256_split(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,

@@ -26,7 +26,6 @@
 namespace hv {
 namespace {
 
-constexpr int kMaxPairs = 2;
 constexpr int kGroups = 40;  // 80 schedule words, two per 16-byte LDS entry
 
 __device__ __forceinline__ uint32_t block_valid(uint32_t nfull, uint32_t r, uint32_t b) {
@@ -228,14 +227,9 @@ __global__ void __launch_bounds__(128 * kPairs) sha384_split_kernel(const LeafDe
 
 hipError_t launch_sha384_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                               hipStream_t s, bool background) {
-    const int choice = leaf_kernel_choice();
-    const uint64_t cus = device_cus();
-    // as for SHA-256: the two-wave kernel while every CU holds one workgroup
-    // at most, the one-wave kernel beyond that and for background work
-    if (choice == 1 || (choice == 0 && (background || n_slots > 64 * kMaxPairs * cus)))
-        return launch_sha384_leaves(desc, n_slots, out_bound, digests, s);
-    const bool two_pairs = choice == 3 || n_slots > 64 * cus;
-    return launch_sha384_split(desc, n_slots, out_bound, digests, two_pairs, s);
+    const int k = leaf_kernel_for(n_slots, background);  // the same rule as SHA-256's
+    if (k == 1) return launch_sha384_leaves(desc, n_slots, out_bound, digests, s);
+    return launch_sha384_split(desc, n_slots, out_bound, digests, k == 3, s);
 }
 
 hipError_t launch_sha384_split(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,

@@ -46,7 +46,7 @@ EXPORTS = (
     "hv_merkle_reduce", "hv_verify_workspace_bytes", "hv_verify_root", "hv_compare_roots",
     "hv_hash_chunks_alg", "hv_merkle_workspace_bytes_alg", "hv_merkle_reduce_alg", "hv_verify_root_alg",
     "hv_compare_roots_alg", "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
-    "hv_leaf_schedule", "hv_set_leaf_kernel",  # include/hv_inspect.h
+    "hv_leaf_schedule", "hv_set_leaf_kernel", "hv_leaf_kernel_for",  # include/hv_inspect.h
     "hv_mb_valu", "hv_mb_sha256", "hv_mb_valu64", "hv_mb_sha384", "hv_mb_op_rate",
     "hv_mb_hbm_read",  # include/hv_microbench.h
     "hv_stream_workspace_bytes", "hv_hash_host_chunks", "hv_hash_host_chunks_alg",  # include/hv_stream.h
@@ -121,6 +121,7 @@ def _load():
         "hv_leaf_kernel_ms": ([vp], ctypes.c_int),
         "hv_leaf_schedule": ([vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
         "hv_set_leaf_kernel": ([ctypes.c_int], ctypes.c_int),
+        "hv_leaf_kernel_for": ([ctypes.c_uint64, ctypes.c_void_p], ctypes.c_int),
         "hv_mb_valu": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_hbm_read": ([vp, u64, vp, u32, vp], ctypes.c_int),
         "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
@@ -472,6 +473,14 @@ def set_leaf_kernel(choice: str):
     """Leaf kernel (SHA-256 and SHA-384) for this thread: "auto", "one-wave", "two-wave" or
     "two-wave-compact" (two producer/consumer pairs per workgroup); digests do not depend on it."""
     _check(lib.hv_set_leaf_kernel({"auto": 0, "one-wave": 1, "two-wave": 2, "two-wave-compact": 3}[choice]))
+
+
+def leaf_kernel_for(n_leaves: int) -> str:
+    """The leaf kernel a hash call over n_leaves leaves runs on the current device under this thread's
+    choice: "one-wave", "two-wave" or "two-wave-compact" (two producer/consumer pairs per workgroup)."""
+    k = ctypes.c_int(0)
+    _check(lib.hv_leaf_kernel_for(int(n_leaves), ctypes.byref(k)))
+    return {1: "one-wave", 2: "two-wave", 3: "two-wave-compact"}[k.value]
 
 
 def set_kernel_timing(enable: bool):

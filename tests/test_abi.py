@@ -386,3 +386,9 @@ def test_leaf_kernel_choice_is_validated():
         assert hv.lib.hv_set_leaf_kernel(ok) == hv.HV_OK
     with pytest.raises(KeyError):
         hv.set_leaf_kernel("fast")
+    # forced choices need no device to answer; NULL output is rejected
+    for name in ("one-wave", "two-wave-compact"):
+        hv.set_leaf_kernel(name)
+        assert hv.leaf_kernel_for(100) == name
+    hv.set_leaf_kernel("auto")
+    assert hv.lib.hv_leaf_kernel_for(10, None) == hv.HV_ERR_INVALID_ARG

@@ -157,6 +157,17 @@ def leaf_kernel():
     hv.set_leaf_kernel("auto")
 
 
+def test_automatic_leaf_kernel_choice_by_leaf_count(leaf_kernel):
+    # the two-wave kernel while every CU holds at most one workgroup (one pair
+    # up to 64 leaves per CU, two up to 128), the one-wave kernel beyond
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    leaf_kernel("auto")
+    assert [hv.leaf_kernel_for(n) for n in (1, 64 * cus, 64 * cus + 1, 128 * cus, 128 * cus + 1)] == \
+        ["two-wave", "two-wave", "two-wave-compact", "two-wave-compact", "one-wave"]
+    leaf_kernel("one-wave")
+    assert hv.leaf_kernel_for(10) == "one-wave"
+
+
 @pytest.mark.parametrize("choice", ["one-wave", "two-wave", "two-wave-compact"])
 @pytest.mark.parametrize("align_off", [0, 3])
 @pytest.mark.parametrize("C", [64, 4096, 0])
