@@ -704,8 +704,12 @@ class Monitor:
         arr = _msg_array(ptrs, lens)
         n = len(arr)
         self.plan = hv_monitor_plan()
-        self.plan_mem = Workspace(self.device).get(lib.hv_monitor_plan_bytes(n))
         self.stream = stream or torch.cuda.Stream(self.device)
+        # the monitor's buffers are allocated on its own stream, which is the
+        # only stream that uses them: the allocator then reuses their memory
+        # in that stream's order, and the monitor never waits on other work
+        with torch.cuda.stream(self.stream):
+            self.plan_mem = Workspace(self.device).get(lib.hv_monitor_plan_bytes(n))
         _check(lib.hv_monitor_init(code, arr.ctypes.data if n else None, n, chunk_bytes, self.plan_mem.data_ptr(),
                                    self.plan_mem.numel(), ctypes.byref(self.plan), self.stream.cuda_stream))
         self.n_leaves = int(self.plan.n_leaves)
@@ -713,8 +717,9 @@ class Monitor:
             raise ValueError(f"ref_digests must be [{self.n_leaves}, {D}]")
         self.ref = ref_digests
         self.slice = max(1, min(int(slice_leaves), max(self.n_leaves, 1)))
-        self.ws = Workspace(self.device).get(lib.hv_monitor_scan_workspace_bytes(code, self.slice))
-        self.results = torch.empty((ring, 2), dtype=torch.int64, device=self.device)
+        with torch.cuda.stream(self.stream):
+            self.ws = Workspace(self.device).get(lib.hv_monitor_scan_workspace_bytes(code, self.slice))
+            self.results = torch.empty((ring, 2), dtype=torch.int64, device=self.device)
         self.host = torch.empty((ring, 2), dtype=torch.int64, pin_memory=True)
         self.events = [None] * ring
         self.ranges = [None] * ring
@@ -732,8 +737,11 @@ class Monitor:
         while self.read <= self.issued - ring:  # the slot's previous result is still unread
             self.poll(wait=True, limit=1)
         res = self.results[slot]
-        ws = self.ws if count <= self.slice else Workspace(self.device).get(
-            lib.hv_monitor_scan_workspace_bytes(_alg(self.alg)[0], count))
+        if count <= self.slice:
+            ws = self.ws
+        else:  # a one-off larger slice: scratch from the monitor stream's own pool
+            with torch.cuda.stream(self.stream):
+                ws = Workspace(self.device).get(lib.hv_monitor_scan_workspace_bytes(_alg(self.alg)[0], count))
         _check(lib.hv_monitor_scan(ctypes.byref(self.plan), first, count, self.ref.data_ptr(),
                                    slice_digests.data_ptr() if slice_digests is not None else None,
                                    res.data_ptr(), ws.data_ptr(), ws.numel(), self.stream.cuda_stream))
