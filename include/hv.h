@@ -144,8 +144,9 @@ size_t hv_verify_workspace_bytes(void);
  * The comparison runs on the GPU over all 32 bytes without an early exit;
  * only the 4-byte flag crosses to the host.
  *   root:     device, 32 bytes.   expected: host, 32 bytes.   match: host.
- *   workspace: device, >= hv_verify_workspace_bytes() bytes.
- * Errors: HV_ERR_INVALID_ARG for NULL pointers; HV_ERR_WORKSPACE; HV_ERR_HIP. */
+ *   workspace: device, >= hv_verify_workspace_bytes() bytes, 4-byte aligned.
+ * Errors: HV_ERR_INVALID_ARG for NULL pointers; HV_ERR_WORKSPACE for a
+ * missing, short or misaligned workspace; HV_ERR_HIP. */
 hv_status hv_verify_root(const uint8_t* root, const uint8_t expected[32], int* match,
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 

@@ -59,7 +59,8 @@ size_t hv_monitor_plan_bytes(uint32_t n_msgs);
 hv_status hv_monitor_init(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, void* plan_memory,
                           size_t plan_bytes, hv_monitor_plan* plan, hipStream_t stream);
 
-/* Scratch bytes of a scan of up to max_slice leaves. */
+/* Scratch bytes of a scan of up to max_slice leaves; 0 (and hv_last_error
+ * set) for an unknown algorithm. */
 size_t hv_monitor_scan_workspace_bytes(hv_alg alg, uint64_t max_slice);
 
 /* One scan (asynchronous on `stream`; no host synchronisation, no upload,

@@ -326,6 +326,7 @@ hv_status hv_verify_root_alg(hv_alg alg, const uint8_t* root, const uint8_t* exp
         return fail(HV_ERR_INVALID_ARG, "root, expected and match must be non-NULL");
     if (workspace == nullptr || workspace_bytes < hv_verify_workspace_bytes())
         return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes", hv_verify_workspace_bytes());
+    if ((uintptr_t)workspace % 4 != 0) return fail(HV_ERR_WORKSPACE, "workspace is not 4-byte aligned");
     uint32_t* flag = static_cast<uint32_t*>(workspace);
     hipError_t e = hv::launch_verify_root(root, expected, digest_bytes(alg), flag, stream);
     if (e != hipSuccess) return hip_fail(e, "verify kernel");

@@ -91,6 +91,10 @@ hv_status hv_monitor_init(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint6
 }
 
 size_t hv_monitor_scan_workspace_bytes(hv_alg alg, uint64_t max_slice) {
+    if (!known(alg)) {
+        (void)fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+        return 0;
+    }
     return scan_layout(nullptr, digest_size(alg), max_slice).bytes;
 }
 

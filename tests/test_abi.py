@@ -145,6 +145,8 @@ def test_verify_rejects_before_launch():
     m = ctypes.c_int(0)
     assert hv.lib.hv_verify_root(None, exp, ctypes.byref(m), 0x1000, 256, None) == hv.HV_ERR_INVALID_ARG
     assert hv.lib.hv_verify_root(0x1000, exp, ctypes.byref(m), None, 256, None) == hv.HV_ERR_WORKSPACE
+    assert hv.lib.hv_verify_root(0x1000, exp, ctypes.byref(m), 0x1002, 256, None) == hv.HV_ERR_WORKSPACE
+    assert b"aligned" in hv.lib.hv_last_error()
     assert hv.lib.hv_compare_roots(None, None, 3, None, None) == hv.HV_ERR_INVALID_ARG
 
 
@@ -247,6 +249,7 @@ def test_monitor_rejects_before_launch():
     plan = hv.hv_monitor_plan(0x100000, 0, 2, 64, 17)
     ws = hv.lib.hv_monitor_scan_workspace_bytes(0, 17)
     assert ws >= 17 * (24 + 32) and hv.lib.hv_monitor_scan_workspace_bytes(1, 17) > ws
+    assert hv.lib.hv_monitor_scan_workspace_bytes(2, 17) == 0 and b"unknown algorithm" in hv.lib.hv_last_error()
     scan = lambda pl, first, n, ref=0x200000, out=None, res=0x300000, w=0x400000, wb=ws: \
         hv.lib.hv_monitor_scan(pl, first, n, ref, out, res, w, wb, None)
     assert scan(None, 0, 1) == hv.HV_ERR_INVALID_ARG
