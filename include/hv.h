@@ -85,8 +85,9 @@ enum { HV_SHA256 = 0, HV_SHA384 = 1 };
  *   seg_offsets: optional (may be NULL), n_msgs + 1 entries: seg_offsets[0] = 0,
  *                seg_offsets[m+1] - seg_offsets[m] = leaves of message m.
  *   n_leaves:    required, total leaves.
- * A single chunk may hold at most 2^38 - 64 bytes (256 GiB, more than one
- * GPU's memory).
+ * A single chunk may hold at most 2^37 bytes (128 GiB), and one call at most
+ * 2^31 leaves (every call of this library that takes a message set or a
+ * segmented node array rejects more).
  * Errors: HV_ERR_INVALID_ARG for msgs == NULL with n_msgs > 0, a NULL data
  * pointer with nbytes > 0, a bad C, a chunk over the size limit, a NULL
  * n_leaves, or a count overflow. */
@@ -131,7 +132,8 @@ size_t hv_merkle_workspace_bytes(uint64_t n_nodes, uint32_t n_seg);
  * The host plans ceil(depth / 9) launches from seg_offsets and uploads that
  * plan before returning (so the call returns once the stream has reached it).
  * Errors: HV_ERR_INVALID_ARG for n_seg == 0, NULL or misaligned pointers,
- * offsets that do not start at 0 or decrease; HV_ERR_WORKSPACE; HV_ERR_HIP. */
+ * offsets that do not start at 0 or decrease, more than 2^31 entries;
+ * HV_ERR_WORKSPACE; HV_ERR_HIP. */
 hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg,
                            uint8_t* roots, void* workspace, size_t workspace_bytes,
                            hipStream_t stream);

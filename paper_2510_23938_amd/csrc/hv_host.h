@@ -14,11 +14,14 @@ namespace hvh {
 constexpr size_t kAlign = 256;
 inline size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Largest leaf count one call accepts: the hash grid is 256 lanes per block
-// in a 32-bit block index.
-constexpr uint64_t kMaxLeaves = (uint64_t)1 << 38;
-// Largest chunk: the leaf kernel counts a chunk's 64-byte blocks in 32 bits.
-constexpr uint64_t kMaxChunkBytes = ((uint64_t)1 << 38) - 64;
+// Largest leaf (or tree entry) count one call accepts.  It keeps the kernels'
+// 32-bit grid-stride indices below 2^32 and is far above what fits in HBM
+// (every leaf takes a 24-byte table entry and its digest besides its bytes).
+constexpr uint64_t kMaxLeaves = (uint64_t)1 << 31;
+// Largest chunk: the leaf kernels count a chunk's 64-byte blocks, padding
+// blocks included, in 32 bits; 2^31 whole blocks leave room for the padding
+// and for the kernels' rounding of block counts to pairs.
+constexpr uint64_t kMaxChunkBytes = (uint64_t)1 << 37;
 
 // Carves consecutive 256-byte-aligned regions out of a workspace.
 struct Carver {

@@ -31,6 +31,11 @@ using Pair = ulonglong2;
 
 constexpr int kSortBuckets = 4096;   // block-count classes of the tail sort
 
+// Leaf launchers split a call into launches of at most this many leaf-table
+// slots, so a grid stays below a dispatch's 2^32 work-items at two lanes per
+// slot (the two-wave kernels).
+constexpr uint64_t kMaxSlotsPerLaunch = (uint64_t)1 << 30;
+
 // Scheduler (sched.hip).
 hipError_t launch_fill_u64(uint64_t* p, size_t n, uint64_t v, hipStream_t s);
 hipError_t launch_sched_count(const MsgDesc* msgs, uint32_t n, uint64_t C, Pair* cnt, hipStream_t s);

@@ -53,7 +53,8 @@ __device__ __forceinline__ void wait_lgkm_all() { __builtin_amdgcn_s_waitcnt(0xC
 
 // Whole blocks of the wave's 64 chunks (every lane's chunk 16-byte aligned),
 // staged through this wave's 8 KB LDS row buffer.  nfull: this lane's whole
-// blocks (< 2^32: a chunk this long would not fit in HBM).
+// blocks (at most 2^31 under the library's chunk-size limit, so the block
+// counts below cannot wrap).
 __device__ __forceinline__ void full_blocks_lds(uint32_t H[8], uint64_t src, uint32_t nfull, uint8_t* rows) {
     const uint32_t lane = threadIdx.x & 63;
     uint32_t nmax = nfull, nmin = nfull;
@@ -198,10 +199,14 @@ __global__ void __launch_bounds__(kThreads) sha256_leaves_kernel(const LeafDesc*
 
 hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                                 hipStream_t s) {
-    if (n_slots == 0) return hipSuccess;
-    const uint64_t blocks = (n_slots + kThreads - 1) / kThreads;
-    sha256_leaves_kernel<<<(unsigned)blocks, kThreads, 0, s>>>(desc, n_slots, out_bound, digests);
-    return hipGetLastError();
+    for (uint64_t base = 0; base < n_slots; base += kMaxSlotsPerLaunch) {
+        const uint64_t n = n_slots - base < kMaxSlotsPerLaunch ? n_slots - base : kMaxSlotsPerLaunch;
+        sha256_leaves_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, s>>>(desc + base, n, out_bound,
+                                                                                          digests);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace hv

@@ -32,7 +32,7 @@ __device__ __forceinline__ void block_from(const uint4 r[8], uint64_t W[16]) {
 }
 
 // Whole 128-byte blocks of the wave's 64 chunks (all 16-byte aligned), staged
-// through this wave's 8 KB LDS rows; nfull < 2^32 (the chunk-size limit).
+// through this wave's 8 KB LDS rows; nfull <= 2^30 (the chunk-size limit).
 __device__ __forceinline__ void full_blocks_lds(uint64_t H[8], uint64_t src, uint32_t nfull, uint8_t* rows) {
     const uint32_t lane = threadIdx.x & 63;
     uint32_t nmax = nfull, nmin = nfull;
@@ -170,10 +170,14 @@ __global__ void __launch_bounds__(kThreads) sha384_leaves_kernel(const LeafDesc*
 
 hipError_t launch_sha384_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                                 hipStream_t s) {
-    if (n_slots == 0) return hipSuccess;
-    const uint64_t blocks = (n_slots + kThreads - 1) / kThreads;
-    sha384_leaves_kernel<<<(unsigned)blocks, kThreads, 0, s>>>(desc, n_slots, out_bound, digests);
-    return hipGetLastError();
+    for (uint64_t base = 0; base < n_slots; base += kMaxSlotsPerLaunch) {
+        const uint64_t n = n_slots - base < kMaxSlotsPerLaunch ? n_slots - base : kMaxSlotsPerLaunch;
+        sha384_leaves_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, s>>>(desc + base, n, out_bound,
+                                                                                          digests);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace hv

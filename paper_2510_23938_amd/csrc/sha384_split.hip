@@ -234,14 +234,16 @@ hipError_t launch_sha384_auto(const LeafDesc* desc, uint64_t n_slots, uint64_t o
 
 hipError_t launch_sha384_split(const LeafDesc* desc, uint64_t n_slots, uint64_t out_bound, uint8_t* digests,
                                bool two_pairs, hipStream_t s) {
-    if (n_slots == 0) return hipSuccess;
-    if (!two_pairs) {
-        sha384_split_kernel<1><<<(unsigned)((n_slots + 63) / 64), 128, 0, s>>>(desc, n_slots, out_bound, digests);
-    } else {
-        const uint64_t blocks = (n_slots + 127) / 128;
-        sha384_split_kernel<2><<<(unsigned)blocks, 256, 0, s>>>(desc, n_slots, out_bound, digests);
+    for (uint64_t base = 0; base < n_slots; base += kMaxSlotsPerLaunch) {
+        const uint64_t n = n_slots - base < kMaxSlotsPerLaunch ? n_slots - base : kMaxSlotsPerLaunch;
+        if (!two_pairs)
+            sha384_split_kernel<1><<<(unsigned)((n + 63) / 64), 128, 0, s>>>(desc + base, n, out_bound, digests);
+        else
+            sha384_split_kernel<2><<<(unsigned)((n + 127) / 128), 256, 0, s>>>(desc + base, n, out_bound, digests);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace hv

@@ -180,6 +180,29 @@ def _stream(device=None) -> int:
     return torch.cuda.current_stream(device).cuda_stream
 
 
+def _dev(device) -> torch.device:
+    """``device`` with its index filled in (the current device for a bare "cuda")."""
+    d = torch.device(device)
+    return d if d.index is not None else torch.device(d.type, torch.cuda.current_device())
+
+
+def _buffer(t, nbytes: int, what: str, device) -> int:
+    """Data pointer of ``t`` once it is known to be a contiguous tensor on ``device``
+    holding at least ``nbytes`` bytes.  The library trusts the pointers it is
+    given, so a short or misplaced buffer would be overrun on the GPU: it is
+    refused here instead."""
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if _dev(t.device) != _dev(device):
+        raise ValueError(f"{what} is on {t.device}, but the call runs on {_dev(device)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{what} holds {have} bytes; the call needs {nbytes}")
+    return t.data_ptr()
+
+
 class Workspace:
     """A growable device byte buffer handed to the library as scratch."""
 
@@ -268,8 +291,9 @@ def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace |
     dev = torch.device(device)
     if out is None:
         out = torch.empty((n_leaves, D), dtype=torch.uint8, device=dev)
+    out_ptr = _buffer(out, n_leaves * D, "out", dev)
     ws = (workspace or Workspace(dev)).get(lib.hv_hash_workspace_bytes(n, n_leaves))
-    _check(_hash_call(alg, arr.ctypes.data if n else None, n, chunk_bytes, out.data_ptr() if n_leaves else None, ws,
+    _check(_hash_call(alg, arr.ctypes.data if n else None, n, chunk_bytes, out_ptr if n_leaves else None, ws,
                       _stream(dev)))
     return out, seg
 
@@ -319,11 +343,15 @@ def hv_merkle_reduce(nodes: torch.Tensor, seg_offsets, workspace: Workspace | No
     _, D = _alg(alg)
     seg = np.ascontiguousarray(seg_offsets, dtype=np.uint64)
     n_seg = len(seg) - 1
+    if n_seg < 1:
+        raise ValueError("seg_offsets needs at least two entries (one segment)")
+    nodes_ptr = _buffer(nodes, int(seg[-1]) * D, "nodes", nodes.device)
     if out is None:
-        out = torch.empty((max(n_seg, 0), D), dtype=torch.uint8, device=nodes.device)
+        out = torch.empty((n_seg, D), dtype=torch.uint8, device=nodes.device)
+    out_ptr = _buffer(out, n_seg * D, "out", nodes.device)
     ws = (workspace or Workspace(nodes.device)).get(_merkle_ws_bytes(alg, int(seg[-1]), n_seg))
-    _check(_merkle_call(alg, nodes.data_ptr() if nodes.numel() else None, seg.ctypes.data, n_seg,
-                        out.data_ptr() if n_seg else None, ws, _stream(nodes.device)))
+    _check(_merkle_call(alg, nodes_ptr if nodes.numel() else None, seg.ctypes.data, n_seg, out_ptr, ws,
+                        _stream(nodes.device)))
     return out
 
 
@@ -335,13 +363,14 @@ def hv_verify_root(root: torch.Tensor, expected: bytes, workspace: Workspace | N
     if len(expected) != D:
         raise ValueError(f"expected root must be {D} bytes for {alg}, got {len(expected)}")
     exp = (ctypes.c_uint8 * D).from_buffer_copy(expected)
+    root_ptr = _buffer(root, D, "root", root.device)
     match = ctypes.c_int(-1)
     ws = (workspace or Workspace(root.device)).get(lib.hv_verify_workspace_bytes())
     if code == HV_SHA256:
-        st = lib.hv_verify_root(root.data_ptr(), exp, ctypes.byref(match), ws.data_ptr(), ws.numel(),
+        st = lib.hv_verify_root(root_ptr, exp, ctypes.byref(match), ws.data_ptr(), ws.numel(),
                                 _stream(root.device))
     else:
-        st = lib.hv_verify_root_alg(code, root.data_ptr(), exp, ctypes.byref(match), ws.data_ptr(), ws.numel(),
+        st = lib.hv_verify_root_alg(code, root_ptr, exp, ctypes.byref(match), ws.data_ptr(), ws.numel(),
                                     _stream(root.device))
     _check(st)
     return match.value == 1
@@ -353,6 +382,8 @@ def hv_compare_roots(roots: torch.Tensor, expected: torch.Tensor, alg: str = "sh
     n = roots.shape[0]
     if roots.shape != (n, D) or expected.shape != (n, D):
         raise ValueError(f"roots and expected must both be [n, {D}] for {alg}")
+    _buffer(roots, n * D, "roots", roots.device)
+    _buffer(expected, n * D, "expected", roots.device)
     mism = torch.empty(n, dtype=torch.int32, device=roots.device)
     if code == HV_SHA256:
         st = lib.hv_compare_roots(roots.data_ptr(), expected.data_ptr(), n, mism.data_ptr(), _stream(roots.device))
@@ -616,6 +647,8 @@ class Pipeline:
 
     def replay(self, expected: bytes | None = None) -> bool:
         """Replay the captured pass (against ``expected`` if given, else the captured one); returns the verdict."""
+        if self.graph is None:
+            raise RuntimeError("nothing captured: call capture() before replay()")
         if expected is not None:
             self.set_expected(expected)
         self.graph.replay()
@@ -635,19 +668,23 @@ class Tree:
         nbytes = lib.hv_tree_bytes_alg(self.code, self.seg.ctypes.data, self.n_seg)
         if nbytes == 0:
             raise HVError(HV_ERR_INVALID_ARG, lib.hv_last_error().decode("utf-8", "replace"))
+        self.D, self.n = D, int(self.seg[-1])
+        leaves_ptr = _buffer(leaf_digests, self.n * D, "leaf_digests", self.device)
         self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
         self.roots = roots if roots is not None else torch.empty((self.n_seg, D), dtype=torch.uint8,
                                                                  device=self.device)
+        _buffer(self.roots, self.n_seg * D, "roots", self.device)
         self.ws = Workspace(self.device)
-        _check(lib.hv_tree_build_alg(self.code, leaf_digests.data_ptr() if leaf_digests.numel() else None,
+        _check(lib.hv_tree_build_alg(self.code, leaves_ptr if leaf_digests.numel() else None,
                                      self.seg.ctypes.data, self.n_seg, self.buf.data_ptr(), self.buf.numel(),
                                      self.roots.data_ptr(), _stream(self.device)))
 
     def update(self, leaf_digests: torch.Tensor, dirty) -> torch.Tensor:
         """Recompute the branches above the listed leaves (sorted unique leaf numbers); returns roots."""
         d = np.ascontiguousarray(dirty, dtype=np.uint64)
+        leaves_ptr = _buffer(leaf_digests, self.n * self.D, "leaf_digests", self.device)
         ws = self.ws.get(lib.hv_tree_update_workspace_bytes(len(d)))
-        _check(lib.hv_tree_update_alg(self.code, leaf_digests.data_ptr() if leaf_digests.numel() else None,
+        _check(lib.hv_tree_update_alg(self.code, leaves_ptr if leaf_digests.numel() else None,
                                       self.seg.ctypes.data, self.n_seg, self.buf.data_ptr(), self.buf.numel(),
                                       d.ctypes.data if len(d) else None, len(d), self.roots.data_ptr(),
                                       ws.data_ptr(), ws.numel(), _stream(self.device)))
@@ -657,15 +694,17 @@ class Tree:
 def hv_rehash_chunks(msgs, chunk_bytes: int, leaves, leaf_digests: torch.Tensor, workspace: Workspace | None = None,
                      alg: str = "sha256"):
     """Recompute leaf_digests[j] for the listed leaf numbers j (sorted, unique) only."""
-    code, _ = _alg(alg)
+    code, D = _alg(alg)
     ptrs, lens = _ptr_len(msgs)
     arr = _msg_array(ptrs, lens)
     n = len(arr)
+    _, n_leaves = _layout_of(arr, chunk_bytes)
+    leaves_ptr = _buffer(leaf_digests, n_leaves * D, "leaf_digests", leaf_digests.device)
     lst = np.ascontiguousarray(leaves, dtype=np.uint64)
     ws = (workspace or Workspace(leaf_digests.device)).get(lib.hv_rehash_workspace_bytes(n, len(lst)))
     _check(lib.hv_rehash_chunks_alg(code, arr.ctypes.data if n else None, n, chunk_bytes,
                                     lst.ctypes.data if len(lst) else None, len(lst),
-                                    leaf_digests.data_ptr() if leaf_digests.numel() else None,
+                                    leaves_ptr if leaf_digests.numel() else None,
                                     ws.data_ptr(), ws.numel(), _stream(leaf_digests.device)))
     return leaf_digests
 
@@ -713,8 +752,9 @@ class Monitor:
         _check(lib.hv_monitor_init(code, arr.ctypes.data if n else None, n, chunk_bytes, self.plan_mem.data_ptr(),
                                    self.plan_mem.numel(), ctypes.byref(self.plan), self.stream.cuda_stream))
         self.n_leaves = int(self.plan.n_leaves)
-        if tuple(ref_digests.shape) != (self.n_leaves, D):
-            raise ValueError(f"ref_digests must be [{self.n_leaves}, {D}]")
+        if tuple(ref_digests.shape) != (self.n_leaves, D) or ref_digests.dtype != torch.uint8:
+            raise ValueError(f"ref_digests must be uint8 [{self.n_leaves}, {D}]")
+        _buffer(ref_digests, self.n_leaves * D, "ref_digests", self.device)
         self.ref = ref_digests
         self.slice = max(1, min(int(slice_leaves), max(self.n_leaves, 1)))
         with torch.cuda.stream(self.stream):
@@ -737,13 +777,15 @@ class Monitor:
         while self.read <= self.issued - ring:  # the slot's previous result is still unread
             self.poll(wait=True, limit=1)
         res = self.results[slot]
+        out_ptr = _buffer(slice_digests, count * self.D, "slice_digests", self.device) \
+            if slice_digests is not None else None
         if count <= self.slice:
             ws = self.ws
         else:  # a one-off larger slice: scratch from the monitor stream's own pool
             with torch.cuda.stream(self.stream):
                 ws = Workspace(self.device).get(lib.hv_monitor_scan_workspace_bytes(_alg(self.alg)[0], count))
         _check(lib.hv_monitor_scan(ctypes.byref(self.plan), first, count, self.ref.data_ptr(),
-                                   slice_digests.data_ptr() if slice_digests is not None else None,
+                                   out_ptr,
                                    res.data_ptr(), ws.data_ptr(), ws.numel(), self.stream.cuda_stream))
         with torch.cuda.stream(self.stream):
             self.host[slot].copy_(res, non_blocking=True)
@@ -863,7 +905,7 @@ def verify(named_tensors, expected: bytes, chunk_bytes: int, alg: str = "sha256"
     """Raise VerificationError unless the manifest root of the tensors equals ``expected``."""
     items = sorted(named_tensors.items(), key=lambda kv: kv[0].encode("utf-8")) \
         if isinstance(named_tensors, dict) else list(named_tensors)
-    v = Verifier(items[0][1].device, alg)
+    v = Verifier(items[0][1].device if items else torch.device("cuda"), alg)
     root = v.manifest_root([t for _, t in items], chunk_bytes)
     if not v.verify_root(root, expected):
         raise VerificationError("model root does not match the expected root")

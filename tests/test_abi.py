@@ -80,14 +80,30 @@ def test_null_data_with_bytes_rejected():
 
 
 def test_chunk_size_limit():
-    big = (1 << 38) - 64
+    big = 1 << 37
     ptrs = np.array([0x1000], dtype=np.uint64)
     assert hv.hv_leaf_layout(ptrs, np.array([big], dtype=np.uint64), 0)[1] == 1
     assert hv.hv_leaf_layout(ptrs, np.array([1 << 40], dtype=np.uint64), 1 << 20)[1] == 1 << 20
-    for lens, C in (([big + 64], 0), ([1 << 39], 1 << 38)):
+    assert hv.hv_leaf_layout(ptrs, np.array([1 << 40], dtype=np.uint64), big)[1] == 8
+    for lens, C in (([big + 1], 0), ([1 << 39], 1 << 38), ([big + 64], big + 64)):
         with pytest.raises(hv.HVError) as e:
             hv.hv_leaf_layout(ptrs, np.array(lens, dtype=np.uint64), C)
         assert e.value.status == hv.HV_ERR_INVALID_ARG and "limit" in str(e.value)
+
+
+def test_leaf_count_limit():
+    # 2^31 leaves per call at most; every check below fails before any HIP call
+    ptrs = np.array([0x1000], dtype=np.uint64)
+    arr = hv._msg_array(ptrs, np.array([(1 << 31) * 64 + 64], dtype=np.uint64))
+    st = hv.lib.hv_hash_chunks(arr.ctypes.data, 1, 64, 0x1000, 0x100000, 1 << 40, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"limit" in hv.lib.hv_last_error()
+    assert hv.lib.hv_plan_bytes(hv.HV_SHA256, arr.ctypes.data, 1, 64, 1) == 0
+    seg = np.array([0, (1 << 31) + 1], dtype=np.uint64)
+    st = hv.lib.hv_merkle_reduce(0x1000, seg.ctypes.data, 1, 0x1000, 0x100000, 1 << 40, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"limit" in hv.lib.hv_last_error()
+    assert hv.lib.hv_tree_bytes(seg.ctypes.data, 1) == 0
+    seg[1] = 1 << 31
+    assert hv.lib.hv_tree_bytes(seg.ctypes.data, 1) > 0
 
 
 def test_null_n_leaves_and_msgs_rejected():
