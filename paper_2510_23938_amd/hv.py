@@ -217,9 +217,31 @@ class Workspace:
         return self.buf
 
 
-def _msg_array(ptrs: np.ndarray, lens: np.ndarray) -> np.ndarray:
-    """hv_msg[n] as a (n, 2) uint64 array (data, nbytes)."""
-    arr = np.empty((len(lens), 2), dtype=np.uint64)
+class HostBuffer:
+    """A growable host byte buffer reused across calls, pinned or pageable.
+
+    For the tables a call hands to the library (the message descriptors) and
+    the segment offsets it plans from: the library reads and uploads them
+    before it returns, so the next call may overwrite them.  Reuse saves the
+    page faults of fresh multi-MB arrays, and a pinned descriptor table
+    uploads by DMA; with 10^6 messages that shortens the host work ahead of
+    each one-shot pass by about a millisecond."""
+
+    def __init__(self, pinned: bool = True):
+        self.pinned = pinned
+        self.buf = None
+
+    def get(self, nbytes: int, dtype=np.uint64) -> np.ndarray:
+        nbytes = int(nbytes)
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.empty(max(nbytes, 4096), dtype=torch.uint8, pin_memory=self.pinned)
+        return self.buf.numpy()[:nbytes].view(dtype)
+
+
+def _msg_array(ptrs: np.ndarray, lens: np.ndarray, host: HostBuffer | None = None) -> np.ndarray:
+    """hv_msg[n] as a (n, 2) uint64 array (data, nbytes), in ``host`` when given."""
+    n = len(lens)
+    arr = host.get(16 * n).reshape(n, 2) if host is not None else np.empty((n, 2), dtype=np.uint64)
     arr[:, 0] = np.asarray(ptrs, dtype=np.uint64)
     arr[:, 1] = np.asarray(lens, dtype=np.uint64)
     return arr
@@ -248,10 +270,10 @@ def hv_leaf_layout(ptrs, lens, chunk_bytes: int):
     return _layout_of(_msg_array(ptrs, lens), chunk_bytes)
 
 
-def _layout_of(arr: np.ndarray, chunk_bytes: int):
-    """(seg_offsets, n_leaves) of an hv_msg array as _msg_array builds it."""
+def _layout_of(arr: np.ndarray, chunk_bytes: int, host: HostBuffer | None = None):
+    """(seg_offsets, n_leaves) of an hv_msg array as _msg_array builds it (seg_offsets in ``host`` when given)."""
     n = len(arr)
-    seg = np.zeros(n + 1, dtype=np.uint64)
+    seg = host.get(8 * (n + 1)) if host is not None else np.zeros(n + 1, dtype=np.uint64)
     n_leaves = ctypes.c_uint64(0)
     _check(lib.hv_leaf_layout(arr.ctypes.data if n else None, n, chunk_bytes, seg.ctypes.data,
                               ctypes.byref(n_leaves)))
@@ -280,13 +302,15 @@ def _merkle_ws_bytes(alg: str, n_nodes: int, n_seg: int) -> int:
 
 
 def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace | None = None, out=None,
-                   alg: str = "sha256"):
+                   alg: str = "sha256", host: HostBuffer | None = None, seg_host: HostBuffer | None = None):
     """Leaf digests of ``msgs`` (tensors, a (ptrs, lens) pair, or an object with
-    ``ptrs``/``lens``): ([n_leaves, D] uint8 device tensor, seg_offsets), D the digest size."""
+    ``ptrs``/``lens``): ([n_leaves, D] uint8 device tensor, seg_offsets), D the digest size.
+    ``host`` holds the descriptor table; with ``seg_host`` the returned seg_offsets
+    live in that buffer, valid until its next use."""
     _, D = _alg(alg)
     ptrs, lens = _ptr_len(msgs)
-    arr = _msg_array(ptrs, lens)
-    seg, n_leaves = _layout_of(arr, chunk_bytes)
+    arr = _msg_array(ptrs, lens, host)
+    seg, n_leaves = _layout_of(arr, chunk_bytes, seg_host)
     n = len(arr)
     dev = torch.device(device)
     if out is None:
@@ -534,26 +558,35 @@ class Verifier:
         self.ws_tree = Workspace(self.device)
         self.ws_manifest = Workspace(self.device)
         self.ws_verify = Workspace(self.device)
+        self.host_msgs = HostBuffer(pinned=True)    # descriptor tables, uploaded by DMA
+        self.host_seg = HostBuffer(pinned=False)    # offsets used only inside one call
+
+    def _leaves(self, msgs, chunk_bytes: int, keep_seg: bool):
+        return hv_hash_chunks(msgs, chunk_bytes, self.device, self.ws_hash, alg=self.alg, host=self.host_msgs,
+                              seg_host=None if keep_seg else self.host_seg)
 
     def leaf_digests(self, msgs, chunk_bytes: int):
-        return hv_hash_chunks(msgs, chunk_bytes, self.device, self.ws_hash, alg=self.alg)
+        return self._leaves(msgs, chunk_bytes, True)
 
-    def roots(self, msgs, chunk_bytes: int):
-        """(per-message roots [n, D], leaf digests, seg_offsets)."""
-        leaves, seg = self.leaf_digests(msgs, chunk_bytes)
+    def _roots(self, msgs, chunk_bytes: int, keep_seg: bool):
+        leaves, seg = self._leaves(msgs, chunk_bytes, keep_seg)
         if len(seg) == 1:  # no messages, no roots (hv_merkle_reduce takes at least one segment)
             return torch.empty((0, self.D), dtype=torch.uint8, device=self.device), leaves, seg
         return hv_merkle_reduce(leaves, seg, self.ws_tree, alg=self.alg), leaves, seg
 
+    def roots(self, msgs, chunk_bytes: int):
+        """(per-message roots [n, D], leaf digests, seg_offsets)."""
+        return self._roots(msgs, chunk_bytes, True)
+
     def manifest_root(self, msgs, chunk_bytes: int) -> torch.Tensor:
         """One root over the per-message roots, in message order ([1, D] device)."""
-        roots, _, _ = self.roots(msgs, chunk_bytes)
+        roots, _, _ = self._roots(msgs, chunk_bytes, False)
         return hv_merkle_reduce(roots, np.array([0, roots.shape[0]], dtype=np.uint64), self.ws_manifest,
                                 alg=self.alg)
 
     def single_tree_root(self, msgs, chunk_bytes: int) -> torch.Tensor:
         """One root over all leaf digests of all messages ([1, D] device)."""
-        leaves, _ = self.leaf_digests(msgs, chunk_bytes)
+        leaves, _ = self._leaves(msgs, chunk_bytes, False)
         return hv_merkle_reduce(leaves, np.array([0, leaves.shape[0]], dtype=np.uint64), self.ws_tree,
                                 alg=self.alg)
 
