@@ -95,7 +95,8 @@ hv_status hv_leaf_layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_byt
                          uint64_t* seg_offsets, uint64_t* n_leaves);
 
 /* Workspace bytes hv_hash_chunks needs for n_msgs messages with n_leaves
- * leaves in total (from hv_leaf_layout). */
+ * leaves in total (from hv_leaf_layout); 0 (and hv_last_error set) for more
+ * than 2^31 leaves. */
 size_t hv_hash_workspace_bytes(uint32_t n_msgs, uint64_t n_leaves);
 
 /* Chunk digests (Algorithm 1's per-chunk GPU hash): leaf_digests[j] =
@@ -115,7 +116,7 @@ hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_byt
                          hipStream_t stream);
 
 /* Workspace bytes hv_merkle_reduce needs for n_nodes entries in n_seg
- * segments. */
+ * segments; 0 (and hv_last_error set) for more than 2^31 entries. */
 size_t hv_merkle_workspace_bytes(uint64_t n_nodes, uint32_t n_seg);
 
 /* Segmented Merkle Tree Hash (RFC 6962 section 2.1; Algorithm 1's "construct

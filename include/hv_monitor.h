@@ -60,7 +60,7 @@ hv_status hv_monitor_init(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint6
                           size_t plan_bytes, hv_monitor_plan* plan, hipStream_t stream);
 
 /* Scratch bytes of a scan of up to max_slice leaves; 0 (and hv_last_error
- * set) for an unknown algorithm. */
+ * set) for an unknown algorithm or more than 2^31 leaves. */
 size_t hv_monitor_scan_workspace_bytes(hv_alg alg, uint64_t max_slice);
 
 /* One scan (asynchronous on `stream`; no host synchronisation, no upload,

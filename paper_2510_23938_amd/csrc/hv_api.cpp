@@ -210,6 +210,10 @@ hv_status hv_leaf_layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_byt
 }
 
 size_t hv_hash_workspace_bytes(uint32_t n_msgs, uint64_t n_leaves) {
+    if (n_leaves > kMaxLeaves) {
+        (void)fail(HV_ERR_INVALID_ARG, "%llu leaves exceed the per-call limit", (unsigned long long)n_leaves);
+        return 0;
+    }
     return hash_layout(nullptr, n_msgs, n_leaves).bytes;
 }
 
@@ -254,6 +258,10 @@ hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_b
 size_t hv_merkle_workspace_bytes_alg(hv_alg alg, uint64_t n_nodes, uint32_t n_seg) {
     if (alg != HV_SHA256 && alg != HV_SHA384) {
         (void)fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+        return 0;
+    }
+    if (n_nodes > kMaxLeaves) {
+        (void)fail(HV_ERR_INVALID_ARG, "%llu entries exceed the per-call limit", (unsigned long long)n_nodes);
         return 0;
     }
     return merkle_layout(nullptr, n_nodes, n_seg, digest_bytes(alg)).bytes;

@@ -95,6 +95,10 @@ size_t hv_monitor_scan_workspace_bytes(hv_alg alg, uint64_t max_slice) {
         (void)fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
         return 0;
     }
+    if (max_slice > kMaxLeaves) {
+        (void)fail(HV_ERR_INVALID_ARG, "%llu leaves exceed the per-call limit", (unsigned long long)max_slice);
+        return 0;
+    }
     return scan_layout(nullptr, digest_size(alg), max_slice).bytes;
 }
 

@@ -102,6 +102,9 @@ def test_leaf_count_limit():
     st = hv.lib.hv_merkle_reduce(0x1000, seg.ctypes.data, 1, 0x1000, 0x100000, 1 << 40, None)
     assert st == hv.HV_ERR_INVALID_ARG and b"limit" in hv.lib.hv_last_error()
     assert hv.lib.hv_tree_bytes(seg.ctypes.data, 1) == 0
+    assert hv.lib.hv_hash_workspace_bytes(1, (1 << 31) + 1) == 0 and hv.lib.hv_hash_workspace_bytes(1, 1 << 31) > 0
+    assert hv.lib.hv_merkle_workspace_bytes((1 << 31) + 1, 1) == 0
+    assert hv.lib.hv_monitor_scan_workspace_bytes(0, 1 << 62) == 0 and b"limit" in hv.lib.hv_last_error()
     seg[1] = 1 << 31
     assert hv.lib.hv_tree_bytes(seg.ctypes.data, 1) > 0
 
