@@ -66,3 +66,19 @@ def test_small_message_workload_schedule_is_sorted():
     assert np.array_equal(table[np.argsort(table[:, 2]), 0], ptrs)
     nblk = (table[:, 1] + 72) // 64
     assert np.all(nblk[:-1] >= nblk[1:])
+
+
+def test_whole_message_classes_across_octaves():
+    # C = 0 with lengths log-uniform from 1 byte to 32 MiB: tails fall in the
+    # exact classes and in the quantised classes of many octaves above them
+    rng = np.random.default_rng(11)
+    lens = np.unique(np.exp(rng.uniform(0, np.log(32 << 20), 80)).astype(np.uint64))
+    lens = np.concatenate([lens, [2047 * 64 - 72, 2048 * 64 - 72, 4096 * 64 - 72, 4097 * 64 - 72]]).astype(np.uint64)
+    buf = torch.empty(int(lens.sum()) + 64 * len(lens), dtype=torch.uint8, device="cuda")
+    starts = np.concatenate([[0], np.cumsum(lens + 64)[:-1]]).astype(np.uint64)
+    ptrs = np.uint64(buf.data_ptr()) + starts
+    table = hv.hv_leaf_schedule((ptrs, lens), 0)
+    assert sorted(tuple(int(x) for x in r) for r in table) == sorted(expected_leaves(ptrs, lens, 0))
+    key = [sort_class(blocks(int(r[1]))) for r in table]
+    assert all(a >= b for a, b in zip(key, key[1:])), "not longest-first"
+    assert len(set(key)) > 40  # many distinct classes exercised
