@@ -137,6 +137,15 @@ def test_70b_random_weights_full_oracle(w70b):
         roots.append(oracle.mth(want))
     assert [bytes(r) for r in pipe.roots.cpu().numpy()] == roots
     assert root == oracle.mth(roots)
+    # the one-shot calls (what the benchmark step times) give the same values
+    v = hv.Verifier(DEV)
+    one_roots, one_leaves, _ = v.roots(wl.msgs, C)
+    top = v.manifest_root(wl.msgs, C)
+    assert np.array_equal(one_leaves.cpu().numpy(), gpu_leaves)
+    assert [bytes(r) for r in one_roots.cpu().numpy()] == roots
+    assert bytes(top.cpu().numpy().reshape(-1)) == root
+    assert v.verify_root(top, root)
+    del v, one_roots, one_leaves, top
 
 
 @pytest.mark.timeout(900)
