@@ -166,7 +166,10 @@ def test_70b_random_weights_sha384_full_oracle(w70b):
     assert [bytes(r) for r in pipe.roots.cpu().numpy()] == roots
     assert root == oracle.mth(roots, "sha384")
     assert pipe.run(root)
-    del pipe
+    v = hv.Verifier(DEV, "sha384")
+    top = v.manifest_root(wl.msgs, C)
+    assert bytes(top.cpu().numpy().reshape(-1)) == root and v.verify_root(top, root)
+    del pipe, v, top
     free()
 
 
