@@ -27,7 +27,7 @@ hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_b
                            void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Leaf-kernel choice for tests and measurements, per calling thread:
- * 0 = automatic (SHA-256 calls with at most 128 leaves per compute unit of
+ * 0 = automatic (calls with at most 128 leaves per compute unit of
  * the current device -- 32768 on MI355X -- use the two-wave kernel, which
  * moves the message schedule to a second wave and shortens each chunk's chain
  * of blocks; others use the one-wave kernel), 1 = always the
