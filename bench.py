@@ -556,6 +556,8 @@ def main():
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
               "the multi-GPU design is described, not run", file=sys.stderr)
         sys.exit(2)
+    if args.steps < 1 or args.warmup < 0 or args.config not in (1, 2, 3, 4, 5):
+        ap.error("--steps must be at least 1, --warmup at least 0 and --config one of 1-5")
 
     import torch
     import workloads as W
