@@ -4,7 +4,6 @@ both padding forms, all alignments, whole-message chunks; RFC 6962 trees with
 48-byte nodes; the on-GPU comparisons over 48 bytes; two model-shaped
 workloads in full.  Expected values come only from ``oracle``.
 """
-import ctypes
 import os
 
 import numpy as np
