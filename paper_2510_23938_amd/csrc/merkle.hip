@@ -15,8 +15,10 @@
 // makes.  One launch therefore takes every segment nine levels up; the host
 // chains ceil(depth / 9) launches, the first of which also forms the leaf
 // hashes as it loads the entries.  Level 1 is formed in registers from the
-// two entries a thread loads; higher levels go through LDS, with idle waves
-// waiting at the barriers.
+// two entries a thread loads.  Levels of more than 64 nodes go through LDS,
+// with idle waves waiting at the barriers; the last six levels of a full tile
+// (64 nodes down to one) stay in wave 0 and exchange children by cross-lane
+// shuffles.
 //
 // The kernel is written once over a node-hash policy: SHA-256 (32-byte nodes;
 // an interior node is two blocks) or SHA-384 (48-byte nodes; leaf and
@@ -28,6 +30,7 @@ namespace hv {
 namespace {
 
 constexpr int kThreads = kTileNodes / 2;  // 256: each thread owns one pair of level 0
+constexpr uint32_t kWave = 64;             // lanes of a wave
 
 __device__ __forceinline__ uint32_t find_segment(const uint64_t* __restrict__ tile_off, uint32_t n_seg, uint64_t tile) {
     uint32_t lo = 0, hi = n_seg;  // tile_off[lo] <= tile < tile_off[hi]
@@ -39,7 +42,7 @@ __device__ __forceinline__ uint32_t find_segment(const uint64_t* __restrict__ ti
 }
 
 template <class T>
-__global__ void __launch_bounds__(kThreads) merkle_tile_kernel(const uint8_t* __restrict__ in, uint8_t* __restrict__ out,
+__global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t* __restrict__ in, uint8_t* __restrict__ out,
                                                                const uint64_t* __restrict__ in_off,
                                                                const uint64_t* __restrict__ tile_off, uint32_t n_seg,
                                                                uint64_t n_tiles, int leaf_mode) {
@@ -55,7 +58,7 @@ __global__ void __launch_bounds__(kThreads) merkle_tile_kernel(const uint8_t* __
         const uint32_t cnt = c > first ? (uint32_t)(c - first < (uint64_t)kTileNodes ? c - first : kTileNodes) : 0u;
         const uint8_t* base = in + NB * (in_off[s] + first);
 
-        uint32_t P[NW];
+        uint32_t P[NW] = {};  // lanes without a node feed zeros to the shuffles
         uint32_t n;  // nodes held in lds after the first level
         if (cnt == 0) {  // empty segment (only ever a first-launch tile)
             if (i == 0) T::empty_hash(P);
@@ -76,10 +79,12 @@ __global__ void __launch_bounds__(kThreads) merkle_tile_kernel(const uint8_t* __
             }
             n = (cnt + 1) / 2;
         }
-        if (i < n) for (int w = 0; w < NW; ++w) lds[w][i] = P[w];
-        __syncthreads();
-        while (n > 1) {
+        // Thread k now holds node k of the current level in P (k < n).  While
+        // the level spans more than one wave, children meet through LDS.
+        while (n > kWave) {
             const uint32_t m = (n + 1) / 2;
+            if (i < n) for (int w = 0; w < NW; ++w) lds[w][i] = P[w];
+            __syncthreads();
             if (i < m) {
                 uint32_t L[NW];
                 for (int w = 0; w < NW; ++w) L[w] = lds[w][2 * i];
@@ -91,15 +96,29 @@ __global__ void __launch_bounds__(kThreads) merkle_tile_kernel(const uint8_t* __
                     for (int w = 0; w < NW; ++w) P[w] = L[w];
                 }
             }
-            __syncthreads();
-            if (i < m) for (int w = 0; w < NW; ++w) lds[w][i] = P[w];
-            __syncthreads();
+            __syncthreads();  // every read of lds is done before the next level writes it
             n = m;
         }
-        if (i == 0) {
-            uint32_t R[NW];
-            for (int w = 0; w < NW; ++w) R[w] = lds[w][0];
-            T::store(out + NB * tile, R);
+        // The rest of the tile lies in wave 0's lanes: children come from
+        // lanes 2k and 2k+1 by cross-lane shuffles, with no barrier.  Every
+        // lane of the wave takes part in the shuffles; only lanes k < m hash.
+        if (i < kWave) {
+            while (n > 1) {
+                const uint32_t m = (n + 1) / 2;
+                uint32_t L[NW], R[NW];
+                for (int w = 0; w < NW; ++w) {
+                    L[w] = __shfl(P[w], (int)((2 * i) & (kWave - 1)));
+                    R[w] = __shfl(P[w], (int)((2 * i + 1) & (kWave - 1)));
+                }
+                if (i < m) {
+                    if (2 * i + 1 < n)
+                        T::node_hash(L, R, P);
+                    else
+                        for (int w = 0; w < NW; ++w) P[w] = L[w];
+                }
+                n = m;
+            }
+            if (i == 0) T::store(out + NB * tile, P);
         }
         __syncthreads();  // lds is reused by the next tile
     }
