@@ -121,6 +121,25 @@ def test_merkle_segments(sizes):
     assert [bytes(r) for r in roots.cpu().numpy()] == want
 
 
+@pytest.mark.parametrize("alg", ["sha256", "sha384"])
+def test_merkle_every_segment_size_up_to_600(alg):
+    # every node count a tile can start from, around the 64-node point where the
+    # kernel moves from LDS levels to wavefront shuffles, and second tiles with
+    # ragged tails; one call over 601 segments of 0..600 entries
+    D = 32 if alg == "sha256" else 48
+    sizes = list(range(601))
+    n = sum(sizes)
+    entries = W.random_bytes(n * D, 250 + D, DEV).view(n, D)
+    seg = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    roots = hv.hv_merkle_reduce(entries, seg, alg=alg)
+    torch.cuda.synchronize()
+    host = entries.cpu().numpy()
+    want = [oracle.mth(host[int(seg[k]):int(seg[k + 1])], alg) for k in range(len(sizes))]
+    got = [bytes(r) for r in roots.cpu().numpy()]
+    bad = [k for k in range(len(sizes)) if got[k] != want[k]]
+    assert not bad, f"{alg}: roots differ for segment sizes {bad[:10]}"
+
+
 def test_verify_and_compare():
     entries = W.random_bytes(5 * 32, 300, DEV).view(5, 32)
     root = hv.hv_merkle_reduce(entries, np.array([0, 5], dtype=np.uint64))
