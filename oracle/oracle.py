@@ -13,8 +13,6 @@ composition of those calls that follows the paper directly:
 * ``manifest_root`` -- the hierarchical roots of the Introduction
   ("Hierarchical Integrity Verification"): a tree over per-tensor roots, in
   the order the caller lists the tensors.
-* ``verify``        -- Algorithm 1's last step: compare the root with the
-  expected value.
 * ``const_seg_root`` -- the same MTH for a message whose bytes are all equal,
   evaluated with memoisation (RFC 6962's recursion only ever meets a few
   distinct sub-lists there), so 100 GB-sized shapes can be pinned in
@@ -174,11 +172,6 @@ def seg_root(data, C: int) -> bytes:
 def manifest_root(messages, C: int) -> bytes:
     """MTH over the per-message roots, in the order given."""
     return mth([seg_root(m, C) for m in messages])
-
-
-def verify(root: bytes, expected: bytes) -> bool:
-    """Algorithm 1's final step: the computed root equals the expected one."""
-    return bytes(root) == bytes(expected)
 
 
 def leaf_digests_mt(messages, C: int, nthreads: int, alg: str = "sha256") -> np.ndarray:

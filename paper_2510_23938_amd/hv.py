@@ -742,16 +742,6 @@ def hv_rehash_chunks(msgs, chunk_bytes: int, leaves, leaf_digests: torch.Tensor,
     return leaf_digests
 
 
-def leaves_of_range(seg_offsets, chunk_bytes: int, msg: int, lo: int, hi: int) -> np.ndarray:
-    """Leaf numbers of the chunks of message `msg` that hold any byte in [lo, hi)."""
-    first = int(seg_offsets[msg])
-    if hi <= lo:
-        return np.zeros(0, dtype=np.uint64)
-    if chunk_bytes == 0:
-        return np.array([first], dtype=np.uint64)
-    return np.arange(first + lo // chunk_bytes, first + (hi - 1) // chunk_bytes + 1, dtype=np.uint64)
-
-
 class Monitor:
     """Continuous runtime monitoring of resident weights (include/hv_monitor.h).
 

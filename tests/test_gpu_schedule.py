@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 import torch
 
-hv = pytest.importorskip("paper_2510_23938_amd.hv")
+from paper_2510_23938_amd import hv  # noqa: E402  (a missing library fails the run, never skips it)
 
 pytestmark = pytest.mark.gpu
 

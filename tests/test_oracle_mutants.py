@@ -9,6 +9,12 @@ an independent bottom-up tree, chunk slices, the threaded driver) in a child
 process.  Every mutant must fail them -- a crash of the child counts as
 caught -- and the unmodified source must pass.  Mistakes are planted only in
 copies, on the CPU; the oracle itself is untouched.
+
+The Python helpers that compose the C primitives (per-message roots from a
+leaf array, the per-message root for either hash, the tree over a digest
+array, the packed driver, the closed form) get the same treatment: copies of
+``oracle/oracle.py`` with one mistake each are imported in a child process
+and run against ``oracle_mutants/py_pins.py``.
 """
 import os
 import subprocess
@@ -19,6 +25,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "hv_oracle.c")
 PINS = os.path.join(ROOT, "tests", "oracle_mutants", "pins.py")
+PY_SRC = os.path.join(ROOT, "oracle", "oracle.py")
+PY_PINS = os.path.join(ROOT, "tests", "oracle_mutants", "py_pins.py")
 
 # (name, text in hv_oracle.c, replacement, which occurrence of the text)
 MUTANTS = [
@@ -87,3 +95,60 @@ def test_planted_mistake_is_caught(name, old, new, occurrence, tmp_path):
     text = plant(open(SRC).read(), old, new, occurrence)
     r = pins_pass(build(text, tmp_path))
     assert r.returncode != 0, f"the pins did not catch: {name}"
+
+
+# (name, text in oracle.py, replacement, which occurrence of the text)
+PY_MUTANTS = [
+    ("per-message roots: position never advances", "        pos += c\n", "", 0),
+    ("per-message roots: one leaf too many", "mth(leaves[pos:pos + c], alg)", "mth(leaves[pos:pos + c + 1], alg)", 0),
+    ("per-message roots: tree always SHA-256", "roots.append(mth(leaves[pos:pos + c], alg))",
+     "roots.append(mth(leaves[pos:pos + c]))", 0),
+    ("seg_root_alg: chunk digests always SHA-256", "return mth(chunk_digests_alg(data, C, alg), alg)",
+     "return mth(chunk_digests_alg(data, C), alg)", 0),
+    ("seg_root_alg: tree always SHA-256", "return mth(chunk_digests_alg(data, C, alg), alg)",
+     "return mth(chunk_digests_alg(data, C, alg))", 0),
+    ("mth: list entries joined in reverse", 'b"".join(entries)', 'b"".join(entries[::-1])', 0),
+    ("mth: array read in memory order, not row order", "e = np.ascontiguousarray(entries, dtype=np.uint8).reshape(-1)",
+     "e = np.frombuffer(np.asarray(entries).base.tobytes() if np.asarray(entries).base is not None "
+     "else np.asarray(entries).tobytes(), dtype=np.uint8)[:np.asarray(entries).size]", 0),
+    ("digest: hashes swapped", 'return sha256(data) if alg == "sha256" else sha384(data)',
+     'return sha384(data)[:32] if alg == "sha256" else sha384(data)', 0),
+    ("packed driver ignores offsets", "ptrs = np.uint64(b.ctypes.data) + offsets",
+     "ptrs = np.uint64(b.ctypes.data) + offsets * np.uint64(0)", 0),
+    ("closed form: tail digest of a whole chunk", "T = sha256(bytes([byte]) * tail) if tail else None",
+     "T = sha256(bytes([byte]) * C) if tail else None", 0),
+    ("closed form: split at the largest power of two <= n", "while k * 2 < n:", "while k * 2 <= n:", 0),
+    ("chunk size not checked against the block", "if n == UINT64_MAX or (C % ALGS[alg][2]):",
+     "if n == UINT64_MAX:", 0),
+]
+
+
+def py_copy(text: str, out_dir) -> str:
+    """A package ``oracle`` under out_dir holding text as oracle.py and the built C oracle."""
+    from oracle import oracle as real
+
+    real._load()  # the copy loads the library built from the unmodified C source
+    pkg = os.path.join(out_dir, "oracle")
+    os.makedirs(pkg)
+    open(os.path.join(pkg, "__init__.py"), "w").close()
+    with open(os.path.join(pkg, "oracle.py"), "w") as f:
+        f.write(text)
+    os.symlink(os.path.join(ROOT, "oracle", "liboracle.so"), os.path.join(pkg, "liboracle.so"))
+    return str(out_dir)
+
+
+def py_pins_pass(pkg_dir: str) -> subprocess.CompletedProcess:
+    return subprocess.run([sys.executable, PY_PINS, pkg_dir], capture_output=True, text=True, timeout=120,
+                          cwd=pkg_dir)
+
+
+def test_unmodified_python_helpers_pass_the_pins(tmp_path):
+    r = py_pins_pass(py_copy(open(PY_SRC).read(), tmp_path))
+    assert r.returncode == 0, r.stderr
+
+
+@pytest.mark.parametrize("name,old,new,occurrence", PY_MUTANTS, ids=[m[0] for m in PY_MUTANTS])
+def test_planted_python_mistake_is_caught(name, old, new, occurrence, tmp_path):
+    text = plant(open(PY_SRC).read(), old, new, occurrence)
+    r = py_pins_pass(py_copy(text, tmp_path))
+    assert r.returncode == 1, f"the pins did not catch: {name} (exit {r.returncode}: {r.stderr[-400:]})"

@@ -55,7 +55,7 @@ def test_recursive_tree_equals_bottom_up(alg, n, seed):
     assert oracle.mth(entries, alg) == bottom_up(entries, alg)
 
 
-hv = pytest.importorskip("paper_2510_23938_amd.hv")
+from paper_2510_23938_amd import hv  # noqa: E402  (a missing library fails the run, never skips it)
 
 
 @settings(max_examples=80, deadline=None)
