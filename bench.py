@@ -15,6 +15,7 @@ oracle timed on a bounded sample of the same bytes on this host.  With
 --alg sha384 every digest and node is SHA-384 (48 bytes, 128-byte blocks).
 """
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -386,7 +387,8 @@ def monitor_bench(args, dev):
         return total
 
     def run_monitor(slice_leaves, ring, stream=None):
-        """Queue ring - 1 scans back to back; returns (monitor, t0 event, [(end event, bytes)])."""
+        """Queue ring - 1 scans back to back; returns (monitor, t0 event, [(end event, bytes)]).
+        ``stream``: a torch stream or a CuMaskedStream (whose close() then closes the monitor)."""
         mon = hv.Monitor(wl.msgs, C, ref, alg, slice_leaves, dev, stream=stream or mon_stream, ring=ring)
         t0 = torch.cuda.Event(enable_timing=True)
         t0.record(mon.stream)
@@ -446,14 +448,13 @@ def monitor_bench(args, dev):
     # Each masked stream holds a hardware queue of its own and a process gets
     # few, so one K per run.
     n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
-    parts = []
-    for K in [args.monitor_partition] if args.monitor_partition else []:
-        mon_cus = list(range(K))  # low CU numbers, which the runtime spreads over the XCDs
+
+    def partitioned(K, inf_p, mon_p):
+        mon_cus = list(range(K))
         rest = [c for c in range(n_cu) if c not in set(mon_cus)]
-        inf_p, mon_p = hv.CuMaskedStream(rest, dev), hv.CuMaskedStream(mon_cus, dev)
         S = len(mon_cus) * 4 * 64 * 2  # two waves per SIMD of the monitor's CUs
         probe = 24
-        mon, t0, ends = run_monitor(S, probe, mon_p.stream)
+        mon, t0, ends = run_monitor(S, probe, mon_p)
         ends[-1][0].synchronize()
         solo = sum(nb for _, nb in ends) / (t0.elapsed_time(ends[-1][0]) / 1e3) / 1e9
         mon.poll(wait=True)
@@ -464,7 +465,7 @@ def monitor_bench(args, dev):
             rest_ms = a.elapsed_time(b) / args.steps
             window = args.steps * rest_ms / 1e3
             n_scans = int(2.0 * window * solo * 1e9 / (S * C)) + 8
-            mon, t0, ends = run_monitor(S, n_scans + 1, mon_p.stream)
+            mon, t0, ends = run_monitor(S, n_scans + 1, mon_p)
             a, b = timed(step, args.steps, inf_p.stream)
             ends[-1][0].synchronize()
             ta, tb = t0.elapsed_time(a), t0.elapsed_time(b)
@@ -484,7 +485,18 @@ def monitor_bench(args, dev):
                               round(slow * min(1.0, sweep / args.monitor_interval), 3) if sweep else None}
             log(f"{len(mon_cus)} monitor CUs: {kind} {alone[kind]:.2f} -> {rest_ms:.2f} on {len(rest)} CUs alone -> "
                 f"{co:.2f} ms/step with the monitor ({slow:+.1f}%), monitor {rate:.0f} GB/s (alone {solo:.0f})")
-        parts.append(part)  # (the masked streams live until the process ends: torch recorded events on them)
+        return part
+
+    parts = []
+    for K in [args.monitor_partition] if args.monitor_partition else []:
+        # low CU numbers, which the runtime spreads over the XCDs
+        inf_p, mon_p = hv.CuMaskedStream(range(K, n_cu), dev), hv.CuMaskedStream(range(K), dev)
+        parts.append(partitioned(K, inf_p, mon_p))
+        # the events and monitors made on the masked streams died with partitioned()'s
+        # frame; the streams are destroyed now, before the process's exit handlers run
+        gc.collect()
+        inf_p.close()
+        mon_p.close()
     # a changed byte is found, at its leaf, by one sweep
     rng = np.random.default_rng(W.seed_of(5) + 11)
     m = int(rng.integers(0, len(wl.msgs)))

@@ -25,8 +25,10 @@ loader does when a model fails its check).
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import weakref
 
 import numpy as np
 import torch  # loads the HIP runtime libhv.so binds to
@@ -766,6 +768,9 @@ class Monitor:
         arr = _msg_array(ptrs, lens)
         n = len(arr)
         self.plan = hv_monitor_plan()
+        if isinstance(stream, CuMaskedStream):
+            stream._users.add(self)  # closed before the masked stream is destroyed
+            stream = stream.stream
         self.stream = stream or torch.cuda.Stream(self.device)
         # the monitor's buffers are allocated on its own stream, which is the
         # only stream that uses them: the allocator then reuses their memory
@@ -795,6 +800,8 @@ class Monitor:
 
     def scan(self, first: int, count: int, slice_digests: torch.Tensor | None = None) -> torch.Tensor:
         """Queue one scan of leaves [first, first + count) on the monitor stream; returns its result slot."""
+        if self.events is None:
+            raise RuntimeError("the monitor is closed")
         ring = len(self.events)
         slot = self.issued % ring
         while self.read <= self.issued - ring:  # the slot's previous result is still unread
@@ -833,10 +840,24 @@ class Monitor:
         for _ in range(-(-self.n_leaves // self.slice)):
             self.step()
 
+    def close(self):
+        """Read the results of every queued scan, then release the events, the
+        pinned result ring and the device buffers, all of which refer to the
+        monitor's stream (idempotent).  A monitor on a CU-masked stream is
+        closed by that stream's ``close`` before the stream is destroyed."""
+        if self.events is None:
+            return
+        self.poll(wait=True)
+        self.stream.synchronize()
+        self.events = self.ranges = None
+        self.host = self.results = self.ws = self.plan_mem = None
+
     def poll(self, wait: bool = False, limit: int | None = None) -> int:
         """Read the results of completed scans, in issue order (waiting for
         each with wait=True), at most ``limit`` of them; returns how many were read."""
         done = 0
+        if self.events is None:
+            return done
         while self.read < self.issued and (limit is None or done < limit):
             slot = self.read % len(self.events)
             ev = self.events[slot]
@@ -864,11 +885,19 @@ def cu_mask_words(cus, n_cu: int) -> np.ndarray:
 
 class CuMaskedStream:
     """A stream whose kernels run only on the given compute units
-    (include/hv_monitor.h), usable wherever torch takes a stream.
+    (include/hv_monitor.h), usable wherever torch takes a stream (``.stream``).
 
-    The stream lives until the process ends, as torch's own streams do:
-    torch records events on the streams it runs work on (pinned-memory copies,
-    ``torch.cuda.Event``), and those must never outlive their stream.
+    Each such stream owns a hardware queue of its own, so it is destroyed
+    explicitly, in this order, by ``close()`` (or by a context manager's exit):
+    the ``Monitor`` objects made on it are closed (their events and pinned
+    result rings released), the whole device is synchronized so every event
+    torch recorded on the stream has completed, torch's pinned-memory cache
+    releases the blocks whose reuse waited on such events, and then the
+    stream is destroyed.  Any other object holding events of this stream
+    (``torch.cuda.Event``, pinned tensors copied on it) must be dropped before
+    ``close()``.  A stream still open when the interpreter exits is closed
+    by an ``atexit`` hook, which runs before the HIP runtime's (and any
+    profiler's) own exit handlers: the queue is never left to their teardown.
     """
 
     def __init__(self, cus, device="cuda"):
@@ -881,8 +910,33 @@ class CuMaskedStream:
             _check(lib.hv_stream_create_cu_masked(words.ctypes.data, len(words), ctypes.byref(handle)))
         self.handle = handle.value
         self.stream = torch.cuda.ExternalStream(self.handle, device=self.device)
+        self._users = weakref.WeakSet()
+        atexit.register(self.close)
+
+    def close(self):
+        """Close the monitors made on this stream, wait for the device, release torch's
+        pinned blocks that waited on the stream, and destroy it (idempotent)."""
+        if self.handle is None:
+            return
+        for mon in list(self._users):
+            mon.close()
+        with torch.cuda.device(self.device):
+            torch.cuda.synchronize(self.device)
+            torch._C._host_emptyCache()
+            _check(lib.hv_stream_destroy(self.handle))
+        self.handle = None
+        self.stream = None
+        atexit.unregister(self.close)
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
 
     def mask(self) -> np.ndarray:
+        if self.handle is None:
+            raise RuntimeError("the stream is closed")
         n_cu = torch.cuda.get_device_properties(self.device).multi_processor_count
         words = np.zeros((n_cu + 31) // 32, dtype=np.uint32)
         _check(lib.hv_stream_cu_mask(self.handle, words.ctypes.data, len(words)))

@@ -222,9 +222,8 @@ def test_cu_masked_streams_with_torch():
     n_cu = torch.cuda.get_device_properties(DEV).multi_processor_count
     with pytest.raises(hv.HVError):
         hv.CuMaskedStream([], DEV)  # a mask with no CU is refused before any stream exists
-    # (the streams live until the process ends: torch records events on them;
     # each masked stream holds a hardware queue of its own, and a process gets
-    # few of those, so these two are the only masked streams the tests keep)
+    # few of those: two at a time here, closed before the next two are made
     mon_s = hv.CuMaskedStream(range(0, 8), DEV)
     rest = hv.CuMaskedStream(range(8, n_cu), DEV)
     assert list(mon_s.mask()) == list(hv.cu_mask_words(range(8), n_cu))
@@ -233,7 +232,7 @@ def test_cu_masked_streams_with_torch():
     buf, host, ptrs, lens, starts = place(lens, 0, seed=904)
     ref_np = oracle.leaf_digests_mt(host_msgs(host, starts, lens), 4096, threads())
     ref = torch.from_numpy(ref_np).to(DEV)
-    mon = hv.Monitor((ptrs, lens), 4096, ref, slice_leaves=256, device=DEV, stream=mon_s.stream)
+    mon = hv.Monitor((ptrs, lens), 4096, ref, slice_leaves=256, device=DEV, stream=mon_s)
     out = torch.empty_like(ref)
     a = torch.randn(1024, 1024, device=DEV)
     want = a @ a
@@ -247,3 +246,21 @@ def test_cu_masked_streams_with_torch():
     rest.stream.synchronize()
     assert mon.mismatches == [] and np.array_equal(out.cpu().numpy(), ref_np)
     assert torch.allclose(got, want, rtol=1e-5, atol=1e-4)
+    # ordered teardown: the monitor made on the stream is closed with it
+    mon_s.close()
+    rest.close()
+    mon_s.close()  # idempotent
+    assert mon_s.handle is None and rest.handle is None
+    with pytest.raises(RuntimeError):
+        mon.scan(0, 1)
+    # their hardware queues are free again: a second pair is made, used, and closed on leaving the block
+    with hv.CuMaskedStream(range(0, 8), DEV) as s2, hv.CuMaskedStream(range(8, n_cu), DEV) as s3:
+        mon2 = hv.Monitor((ptrs, lens), 4096, ref, slice_leaves=512, device=DEV, stream=s2)
+        mon2.sweep()
+        with torch.cuda.stream(s3.stream):
+            got2 = a @ a
+        mon2.poll(wait=True)
+        s3.stream.synchronize()
+        assert mon2.mismatches == [] and mon2.read == -(-mon2.n_leaves // 512)
+        assert torch.allclose(got2, want, rtol=1e-5, atol=1e-4)
+    assert s2.handle is None and s3.handle is None and mon2.events is None

@@ -208,10 +208,12 @@ def test_kernel_timing_covers_the_sha384_kernel():
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("k", [2, 4])
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
 def test_workloads_in_full(k):
-    # 1B-shaped weights (per-tensor roots + manifest, 1 MiB chunks) and 10^6
-    # small messages (whole-message chunks, one root), at their full sizes
+    # at their full sizes: 64 MiB of random bytes (1 MiB chunks, one root),
+    # 1B-shaped weights (per-tensor roots + manifest, 1 MiB chunks), the
+    # 7B-shaped shard files (per-file roots + manifest, 4 MiB chunks) and
+    # 10^6 small messages (whole-message chunks, one root)
     wl = W.workload(k, DEV)
     pipe = hv.Pipeline(wl.msgs, wl.chunk_bytes, "manifest" if wl.manifest else "single", DEV, alg=ALG)
     root = bytes(pipe.compute().cpu().numpy().reshape(-1))
@@ -235,3 +237,5 @@ def test_workloads_in_full(k):
     bad = bytearray(expected)
     bad[47] ^= 1
     assert not pipe.run(bytes(bad))
+    del wl, pipe
+    torch.cuda.empty_cache()
