@@ -23,7 +23,8 @@
  * Conventions for every call:
  *   - Device pointers are caller-owned (typically torch tensor storage).  The
  *     library never allocates device memory: scratch comes from a
- *     caller-provided workspace of the size the *_workspace_bytes call gives.
+ *     caller-provided workspace of the size the *_workspace_bytes call gives
+ *     (hv_hash_chunks_noalloc alone uses a static array of the library's).
  *   - Calls are asynchronous on `stream` unless marked "synchronous".  Input
  *     bytes must stay valid and unmodified until the stream work completes.
  *     Host arrays a call takes (message tables, offset, leaf and dirty lists,
@@ -35,9 +36,10 @@
  *     status nothing was launched (except HV_ERR_HIP, which reports a failed
  *     launch or copy) and hv_last_error() describes the problem.
  *   - A root mismatch is not an error: hv_verify_root returns HV_OK, *match=0.
- *   - No global state except a thread-local error string.  Concurrent calls
- *     on different streams with different workspaces are safe; calls that
- *     share a workspace must be ordered by the caller.
+ *   - No global state except a thread-local error string (and the static
+ *     scratch of hv_hash_chunks_noalloc).  Concurrent calls on different
+ *     streams with different workspaces are safe; calls that share a
+ *     workspace must be ordered by the caller.
  */
 #ifndef HV_H
 #define HV_H
@@ -177,6 +179,31 @@ hv_status hv_verify_root_alg(hv_alg alg, const uint8_t* root, const uint8_t* exp
                              size_t workspace_bytes, hipStream_t stream);
 hv_status hv_compare_roots_alg(hv_alg alg, const uint8_t* roots, const uint8_t* expected, uint32_t n,
                                uint32_t* mismatch, hipStream_t stream);
+
+/* Chunk digests without allocation, for callers that cannot allocate device
+ * memory or pass a workspace (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same operation, digests, layout,
+ * argument checks and errors as hv_hash_chunks_alg with the same arguments;
+ * only the workspace differs: the scheduler's scratch (16 B per message for
+ * the descriptors, 32 B per message for counts and offsets, a 32 KiB tail
+ * histogram and 24 B per leaf for the leaf table, each region rounded up to
+ * 256 B) lives in a static device array of HV_NOALLOC_SCRATCH_BYTES (64 MiB)
+ * inside the library, one per GPU, held from the first call on that GPU until
+ * the process ends.  That covers, e.g., one message of up to 2,794,794 leaves,
+ * or the 723 tensors and 2,153,249 leaves of a 70B-shaped weight set with
+ * 64 KiB chunks.  The call makes no hipMalloc, hipFree or other allocation;
+ * it runs on the GPU that owns `stream`, and, like hv_hash_chunks, uploads
+ * the descriptors before it returns.
+ * Every call on one GPU shares that GPU's array, and each call rewrites what
+ * it reads there: calls whose work may overlap on one GPU (other streams,
+ * other threads) race and must be ordered by the caller.  The leaf-kernel
+ * timing of hv_set_kernel_timing is not recorded.
+ * Errors: those of hv_hash_chunks_alg, and HV_ERR_INVALID_ARG, before any
+ * work is queued, when the message set needs more scratch than the array
+ * holds (hv_last_error() gives both sizes). */
+enum { HV_NOALLOC_SCRATCH_BYTES = 64 << 20 };
+hv_status hv_hash_chunks_noalloc(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                                 uint8_t* leaf_digests, hipStream_t stream);
 
 /* Detail string for the last non-OK status returned on this thread. */
 const char* hv_last_error(void);

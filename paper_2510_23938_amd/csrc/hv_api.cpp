@@ -199,6 +199,30 @@ hv_status schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, bo
 
 }  // namespace
 
+namespace hvh {
+
+hv_status hash_chunks_into(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                           uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, bool timed,
+                           hipStream_t stream) {
+    if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+    if (alg == HV_SHA384 && chunk_bytes % 128 != 0)
+        return fail(HV_ERR_INVALID_ARG, "chunk_bytes = %llu is not 0 or a multiple of 128 (SHA-384 blocks)",
+                    (unsigned long long)chunk_bytes);
+    HashLayout L;
+    uint64_t n_leaves = 0;
+    hv_status st = schedule(msgs, n_msgs, chunk_bytes, true, leaf_digests, workspace, workspace_bytes, stream, &L,
+                            &n_leaves);
+    if (st != HV_OK || n_leaves == 0) return st;
+
+    if (timed && (st = leaf_timing_start(stream)) != HV_OK) return st;
+    const hipError_t e = alg == HV_SHA384 ? hv::launch_sha384_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream)
+                                          : hv::launch_sha256_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream);
+    if (e != hipSuccess) return hip_fail(e, "leaf kernel");
+    return timed ? leaf_timing_stop(stream) : HV_OK;
+}
+
+}  // namespace hvh
+
 extern "C" {
 
 const char* hv_last_error(void) { return g_error; }
@@ -219,21 +243,7 @@ size_t hv_hash_workspace_bytes(uint32_t n_msgs, uint64_t n_leaves) {
 
 hv_status hv_hash_chunks_alg(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
                              uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
-    if (alg == HV_SHA384 && chunk_bytes % 128 != 0)
-        return fail(HV_ERR_INVALID_ARG, "chunk_bytes = %llu is not 0 or a multiple of 128 (SHA-384 blocks)",
-                    (unsigned long long)chunk_bytes);
-    HashLayout L;
-    uint64_t n_leaves = 0;
-    hv_status st = schedule(msgs, n_msgs, chunk_bytes, true, leaf_digests, workspace, workspace_bytes, stream, &L,
-                            &n_leaves);
-    if (st != HV_OK || n_leaves == 0) return st;
-
-    if ((st = leaf_timing_start(stream)) != HV_OK) return st;
-    const hipError_t e = alg == HV_SHA384 ? hv::launch_sha384_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream)
-                                          : hv::launch_sha256_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream);
-    if (e != hipSuccess) return hip_fail(e, "leaf kernel");
-    return leaf_timing_stop(stream);
+    return hash_chunks_into(alg, msgs, n_msgs, chunk_bytes, leaf_digests, workspace, workspace_bytes, true, stream);
 }
 
 hv_status hv_hash_chunks(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, uint8_t* leaf_digests,

@@ -56,6 +56,13 @@ hv_status hip_fail(hipError_t e, const char* what);
 hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_offsets, uint64_t* n_leaves,
                  uint64_t* n_full);
 
+// The body of hv_hash_chunks_alg over a given workspace (validation, descriptor
+// upload, scheduling, leaf kernel); `timed` records the leaf-kernel events of
+// hv_set_kernel_timing when that is on.
+hv_status hash_chunks_into(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
+                           uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, bool timed,
+                           hipStream_t stream);
+
 // Scheduling kernels over device-resident descriptors into L (leaf table in L.desc).
 hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t n_full,
                          uint64_t n_leaves, const HashLayout& L, hipStream_t stream);

@@ -38,6 +38,7 @@ LIB_PATH = os.path.join(_HERE, "libhv.so")
 
 HV_OK, HV_ERR_INVALID_ARG, HV_ERR_WORKSPACE, HV_ERR_HIP = 0, 1, 2, 3
 HV_SHA256, HV_SHA384 = 0, 1
+HV_NOALLOC_SCRATCH_BYTES = 64 << 20  # the static scratch of hv_hash_chunks_noalloc, per GPU
 # hash name -> (hv_alg code, digest bytes)
 ALGS = {"sha256": (HV_SHA256, 32), "sha384": (HV_SHA384, 48)}
 _STATUS = {1: "HV_ERR_INVALID_ARG", 2: "HV_ERR_WORKSPACE", 3: "HV_ERR_HIP"}
@@ -47,7 +48,7 @@ EXPORTS = (
     "hv_leaf_layout", "hv_hash_workspace_bytes", "hv_hash_chunks", "hv_merkle_workspace_bytes",
     "hv_merkle_reduce", "hv_verify_workspace_bytes", "hv_verify_root", "hv_compare_roots",
     "hv_hash_chunks_alg", "hv_merkle_workspace_bytes_alg", "hv_merkle_reduce_alg", "hv_verify_root_alg",
-    "hv_compare_roots_alg", "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
+    "hv_compare_roots_alg", "hv_hash_chunks_noalloc", "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
     "hv_leaf_schedule", "hv_set_leaf_kernel", "hv_leaf_kernel_for",  # include/hv_inspect.h
     "hv_mb_valu", "hv_mb_sha256", "hv_mb_valu64", "hv_mb_sha384", "hv_mb_op_rate",
     "hv_mb_hbm_read",  # include/hv_microbench.h
@@ -118,6 +119,7 @@ def _load():
         "hv_merkle_reduce_alg": ([ctypes.c_int, vp, vp, u32, vp, vp, sz, vp], ctypes.c_int),
         "hv_verify_root_alg": ([ctypes.c_int, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "hv_compare_roots_alg": ([ctypes.c_int, vp, vp, u32, vp, vp], ctypes.c_int),
+        "hv_hash_chunks_noalloc": ([ctypes.c_int, vp, u32, u64, vp, vp], ctypes.c_int),
         "hv_last_error": ([], ctypes.c_char_p),
         "hv_set_kernel_timing": ([ctypes.c_int], ctypes.c_int),
         "hv_leaf_kernel_ms": ([vp], ctypes.c_int),
@@ -321,6 +323,23 @@ def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace |
     ws = (workspace or Workspace(dev)).get(lib.hv_hash_workspace_bytes(n, n_leaves))
     _check(_hash_call(alg, arr.ctypes.data if n else None, n, chunk_bytes, out_ptr if n_leaves else None, ws,
                       _stream(dev)))
+    return out, seg
+
+
+def hv_hash_chunks_noalloc(msgs, chunk_bytes: int, device="cuda", out=None, alg: str = "sha256"):
+    """Leaf digests as ``hv_hash_chunks``, with the library's static scratch in place of a
+    workspace (the C call allocates nothing; ``out`` is allocated here when not given)."""
+    code, D = _alg(alg)
+    ptrs, lens = _ptr_len(msgs)
+    arr = _msg_array(ptrs, lens)
+    seg, n_leaves = _layout_of(arr, chunk_bytes)
+    n = len(arr)
+    dev = torch.device(device)
+    if out is None:
+        out = torch.empty((n_leaves, D), dtype=torch.uint8, device=dev)
+    out_ptr = _buffer(out, n_leaves * D, "out", dev)
+    _check(lib.hv_hash_chunks_noalloc(code, arr.ctypes.data if n else None, n, chunk_bytes,
+                                      out_ptr if n_leaves else None, _stream(dev)))
     return out, seg
 
 

@@ -414,3 +414,33 @@ def test_leaf_kernel_choice_is_validated():
         assert hv.leaf_kernel_for(100) == name
     hv.set_leaf_kernel("auto")
     assert hv.lib.hv_leaf_kernel_for(10, None) == hv.HV_ERR_INVALID_ARG
+
+
+def test_noalloc_refuses_what_its_static_scratch_cannot_hold():
+    # the array's size as the header states it, and the largest single-message set it holds
+    hdr = open(os.path.join(ROOT, "include", "hv.h")).read()
+    assert re.search(r"HV_NOALLOC_SCRATCH_BYTES\s*=\s*64\s*<<\s*20", hdr)
+    assert hv.HV_NOALLOC_SCRATCH_BYTES == 64 << 20
+    n_max = 2_794_794
+    assert hv.lib.hv_hash_workspace_bytes(1, n_max) == hv.HV_NOALLOC_SCRATCH_BYTES
+    assert hv.lib.hv_hash_workspace_bytes(1, n_max + 1) > hv.HV_NOALLOC_SCRATCH_BYTES
+    # a 70B-shaped set (723 tensors, 2,153,249 leaves) fits
+    assert hv.lib.hv_hash_workspace_bytes(723, 2_153_249) <= hv.HV_NOALLOC_SCRATCH_BYTES
+    # checks that fail before the first HIP call (the scratch lookup), so no GPU is needed
+    ptrs, lens = _msgs([64 * (n_max + 1)])
+    arr = hv._msg_array(ptrs, lens)
+    st = hv.lib.hv_hash_chunks_noalloc(hv.HV_SHA256, arr.ctypes.data, 1, 64, 0x1000, None)
+    assert st == hv.HV_ERR_INVALID_ARG and b"static scratch" in hv.lib.hv_last_error()
+    ptrs, lens = _msgs([1000, 64])
+    arr = hv._msg_array(ptrs, lens)
+    p = arr.ctypes.data
+    assert hv.lib.hv_hash_chunks_noalloc(2, p, 2, 64, 0x1000, None) == hv.HV_ERR_INVALID_ARG
+    assert b"unknown algorithm" in hv.lib.hv_last_error()
+    assert hv.lib.hv_hash_chunks_noalloc(hv.HV_SHA384, p, 2, 64, 0x1000, None) == hv.HV_ERR_INVALID_ARG
+    assert b"multiple of 128" in hv.lib.hv_last_error()
+    assert hv.lib.hv_hash_chunks_noalloc(hv.HV_SHA256, p, 2, 96, 0x1000, None) == hv.HV_ERR_INVALID_ARG
+    assert hv.lib.hv_hash_chunks_noalloc(hv.HV_SHA256, p, 2, 64, None, None) == hv.HV_ERR_INVALID_ARG
+    assert b"leaf_digests is NULL" in hv.lib.hv_last_error()
+    assert hv.lib.hv_hash_chunks_noalloc(hv.HV_SHA256, p, 2, 64, 0x1008, None) == hv.HV_ERR_INVALID_ARG
+    assert b"16-byte aligned" in hv.lib.hv_last_error()
+    assert hv.lib.hv_hash_chunks_noalloc(hv.HV_SHA256, None, 2, 64, 0x1000, None) == hv.HV_ERR_INVALID_ARG
