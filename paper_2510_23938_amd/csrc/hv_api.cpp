@@ -118,21 +118,25 @@ MerkleLayout merkle_layout(void* ws, uint64_t n_nodes, uint32_t n_seg, uint32_t 
 namespace hvh {
 
 uint64_t merkle_tiles_bound(uint64_t n_nodes, uint32_t n_seg) {
-    return n_nodes / hv::kTileNodes + (uint64_t)n_seg + 1;
+    // a launch over c entries of a segment writes max(1, ceil(c / w)) <= c / w + 1 nodes
+    const uint64_t w = merkle_grouped(n_nodes) ? (uint64_t)hv::kGroupNodes : (uint64_t)hv::kTileNodes;
+    return n_nodes / w + (uint64_t)n_seg + 1;
 }
 
 hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches) {
     const size_t row = (size_t)n_seg + 1;
     table->assign(seg_offsets, seg_offsets + row);
+    const bool grouped = merkle_grouped(seg_offsets[n_seg]);
     int k = 0;
     for (;;) {
+        const uint64_t w = grouped && k == 0 ? (uint64_t)hv::kGroupNodes : (uint64_t)hv::kTileNodes;
         std::vector<uint64_t> next(row);
         next[0] = 0;
         bool more = false;
         for (uint32_t s = 0; s < n_seg; ++s) {
             const uint64_t* prev = table->data() + (size_t)k * row;
             const uint64_t c = prev[s + 1] - prev[s];
-            const uint64_t tiles = c <= (uint64_t)hv::kTileNodes ? 1 : (c + hv::kTileNodes - 1) / hv::kTileNodes;
+            const uint64_t tiles = c <= w ? 1 : (c + w - 1) / w;
             if (tiles > 1) more = true;
             next[s + 1] = next[s] + tiles;
         }
@@ -142,6 +146,26 @@ hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<u
         if (k == kMaxMerkleLaunches) return fail(HV_ERR_INVALID_ARG, "tree too deep");
     }
     *launches = k;
+    return HV_OK;
+}
+
+hv_status queue_merkle(hv_alg alg, const uint8_t* in, uint8_t* out, const uint64_t* table, uint32_t n_seg,
+                       uint64_t n_nodes, int launches, const uint64_t* outputs, uint8_t* ping, uint8_t* pong,
+                       hipStream_t stream) {
+    const size_t row = (size_t)n_seg + 1;
+    const int a = alg == HV_SHA384 ? hv::kAlgSha384 : hv::kAlgSha256;
+    const bool grouped = merkle_grouped(n_nodes);
+    for (int k = 1; k <= launches; ++k) {
+        uint8_t* dst = k == launches ? out : (k % 2 ? ping : pong);
+        const uint64_t* in_off = table + (size_t)(k - 1) * row;
+        const uint64_t* out_off = table + (size_t)k * row;
+        const hipError_t e = grouped && k == 1
+                                 ? hv::launch_merkle_groups(a, in, dst, in_off, out_off, n_seg, outputs[0], 1, stream)
+                                 : hv::launch_merkle_tiles(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1,
+                                                           stream);
+        if (e != hipSuccess) return hip_fail(e, "merkle kernel");
+        in = dst;
+    }
     return HV_OK;
 }
 
@@ -313,21 +337,12 @@ hv_status hv_merkle_reduce_alg(hv_alg alg, const uint8_t* nodes, const uint64_t*
     if (st != HV_OK) return st;
 
     const MerkleLayout L = merkle_layout(workspace, n_nodes, n_seg, D);
-    hipError_t e = hipMemcpyWithStream(L.table, table.data(), table.size() * sizeof(uint64_t), hipMemcpyHostToDevice,
-                                       stream);
+    const hipError_t e = hipMemcpyWithStream(L.table, table.data(), table.size() * sizeof(uint64_t),
+                                             hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "plan upload");
-    const uint8_t* in = nodes;
-    for (int k = 1; k <= launches; ++k) {
-        uint8_t* out = k == launches ? roots : (k % 2 ? L.ping : L.pong);
-        const uint64_t* in_off = L.table + (size_t)(k - 1) * row;
-        const uint64_t* tile_off = L.table + (size_t)k * row;
-        const uint64_t n_tiles = table[(size_t)k * row + n_seg];
-        if ((e = hv::launch_merkle_tiles(alg == HV_SHA384 ? hv::kAlgSha384 : hv::kAlgSha256, in, out, in_off, tile_off,
-                                         n_seg, n_tiles, k == 1, stream)) != hipSuccess)
-            return hip_fail(e, "merkle kernel");
-        in = out;
-    }
-    return HV_OK;
+    uint64_t outputs[kMaxMerkleLaunches];
+    for (int k = 1; k <= launches; ++k) outputs[k - 1] = table[(size_t)k * row + n_seg];
+    return queue_merkle(alg, nodes, roots, L.table, n_seg, n_nodes, launches, outputs, L.ping, L.pong, stream);
 }
 
 hv_status hv_merkle_reduce(const uint8_t* nodes, const uint64_t* seg_offsets, uint32_t n_seg, uint8_t* roots,

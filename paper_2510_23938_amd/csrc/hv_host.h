@@ -67,18 +67,32 @@ hv_status hash_chunks_into(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint
 hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t n_full,
                          uint64_t n_leaves, const HashLayout& L, hipStream_t stream);
 
-// Segmented Merkle reductions chain launches of 9 levels each (512-node tiles).
-// A 64-bit node count needs at most ceil(64 / 9) = 8 launches.
+// Segmented Merkle reductions chain launches.  A reduction of at least
+// kGroupMinNodes entries starts with a group launch (3 levels in registers,
+// one lane per group of 8 entries: every lane busy on the widest levels);
+// every other launch takes 9 levels (512-node tiles).  A 64-bit node count
+// needs at most 1 + ceil(61 / 9) = 8 launches.
 constexpr int kMaxMerkleLaunches = 8;
+constexpr uint64_t kGroupMinNodes = (uint64_t)1 << 18;
+inline bool merkle_grouped(uint64_t n_nodes) { return n_nodes >= kGroupMinNodes; }
 
 // Host plan of a segmented Merkle reduction over validated segment offsets:
 // `table` gets rows of n_seg + 1 offsets -- row 0 the segment offsets, row k
 // the first output node of each segment after launch k (a segment with c
-// nodes gets max(1, ceil(c / 512)) tiles) -- and `launches` the launch count.
+// nodes gets max(1, ceil(c / w)) outputs, w = 8 for a group launch, else
+// 512) -- and `launches` the launch count.  The first launch is a group
+// launch exactly when merkle_grouped(seg_offsets[n_seg]).
 hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches);
 
 // Nodes any launch of a reduction of n_nodes nodes in n_seg segments writes, at most.
 uint64_t merkle_tiles_bound(uint64_t n_nodes, uint32_t n_seg);
+
+// Queues the launches of a planned reduction: `in` (entries; the first launch
+// forms their leaf hashes) through ping / pong into `out`.  table: the plan's
+// rows on the device; outputs[k]: nodes written by launch k + 1.
+hv_status queue_merkle(hv_alg alg, const uint8_t* in, uint8_t* out, const uint64_t* table, uint32_t n_seg,
+                       uint64_t n_nodes, int launches, const uint64_t* outputs, uint8_t* ping, uint8_t* pong,
+                       hipStream_t stream);
 
 // HIP events around a leaf kernel on `stream` when hv_set_kernel_timing is on
 // for this thread (no-ops otherwise).

@@ -110,6 +110,14 @@ constexpr int kTileNodes = 1 << kTileLevels;
 hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
                                const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode,
                                hipStream_t s);
+// Merkle groups (merkle.hip), the first launch of a large reduction: one lane
+// reduces group g -- up to 2^kGroupLevels consecutive nodes of one segment,
+// starting at a multiple of that -- to one node, in registers.
+constexpr int kGroupLevels = 3;
+constexpr int kGroupNodes = 1 << kGroupLevels;
+hipError_t launch_merkle_groups(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
+                                const uint64_t* grp_off, uint32_t n_seg, uint64_t n_groups, int leaf_mode,
+                                hipStream_t s);
 
 // Persistent tree for incremental updates (tree.hip).
 hipError_t launch_tree_leaf_level(int alg, const uint8_t* digests, uint64_t n, uint8_t* level0, hipStream_t s);

@@ -83,22 +83,6 @@ hv_status prepare(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t C, i
     return HV_OK;
 }
 
-// Merkle launches of one tree: entries `in` (nodes, or leaf digests when the
-// first launch forms leaf hashes) through ping / pong into `out`.
-hv_status reduce(hv_alg alg, const uint8_t* in, uint8_t* out, const uint64_t* table, uint32_t n_seg, uint32_t launches,
-                 const uint64_t* tiles, uint8_t* ping, uint8_t* pong, hipStream_t stream) {
-    const size_t row = (size_t)n_seg + 1;
-    for (uint32_t k = 1; k <= launches; ++k) {
-        uint8_t* dst = k == launches ? out : (k % 2 ? ping : pong);
-        const hipError_t e = hv::launch_merkle_tiles(alg == HV_SHA384 ? hv::kAlgSha384 : hv::kAlgSha256, in, dst,
-                                                     table + (size_t)(k - 1) * row, table + (size_t)k * row, n_seg,
-                                                     tiles[k - 1], k == 1, stream);
-        if (e != hipSuccess) return hip_fail(e, "merkle kernel");
-        in = dst;
-    }
-    return HV_OK;
-}
-
 // Workspace of hv_verify_model: the plan, then its outputs and the comparison buffers.
 struct ModelLayout {
     void* plan;
@@ -209,13 +193,15 @@ hv_status hv_plan_run(const hv_verify_plan* plan, uint8_t* leaf_digests, uint8_t
         if (e != hipSuccess) return hip_fail(e, "leaf kernel");
         if ((st = leaf_timing_stop(stream)) != HV_OK) return st;
     }
-    if (plan->n_seg > 0 && (st = reduce(plan->alg, leaf_digests, roots, P.table[0], plan->n_seg, plan->launches[0],
-                                        plan->tiles[0], P.ping, P.pong, stream)) != HV_OK)
+    // the first tree has n_leaves entries (per-message segments, or one), the manifest one per message
+    if (plan->n_seg > 0 &&
+        (st = queue_merkle(plan->alg, leaf_digests, roots, P.table[0], plan->n_seg, plan->n_leaves,
+                           (int)plan->launches[0], plan->tiles[0], P.ping, P.pong, stream)) != HV_OK)
         return st;
     const uint8_t* top = roots;
     if (plan->manifest) {
-        if ((st = reduce(plan->alg, roots, root, P.table[1], 1, plan->launches[1], plan->tiles[1], P.ping, P.pong,
-                         stream)) != HV_OK)
+        if ((st = queue_merkle(plan->alg, roots, root, P.table[1], 1, plan->n_msgs, (int)plan->launches[1],
+                               plan->tiles[1], P.ping, P.pong, stream)) != HV_OK)
             return st;
         top = root;
     }

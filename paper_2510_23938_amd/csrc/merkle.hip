@@ -13,14 +13,21 @@
 // pair ever straddles two tiles, and the tile's last unpaired node at any level
 // is the segment's last node there -- the same promotion the whole tree
 // makes.  One launch therefore takes every segment nine levels up; the host
-// chains ceil(depth / 9) launches, the first of which also forms the leaf
-// hashes as it loads the entries.  Level 1 is formed in registers from the
+// chains such launches until one node per segment is left, and the first
+// launch of a reduction also forms the leaf hashes as it loads the entries.  Level 1 is formed in registers from the
 // two entries a thread loads.  Levels of more than 64 nodes go through LDS,
 // with idle waves waiting at the barriers; the last six levels of a full tile
 // (64 nodes down to one) stay in wave 0 and exchange children by cross-lane
 // shuffles.
 //
-// The kernel is written once over a node-hash policy: SHA-256 (32-byte nodes;
+// A large reduction (at least 2^18 entries) first runs a group launch (below):
+// one lane per aligned group of 8 entries, three levels in registers, so that
+// the widest levels keep every lane busy; the tile launches then start from
+// the group nodes.  The tile kernel alone leaves lanes idle on its top levels
+// and costs more for the same nodes: on the 70B-shaped set (2.15 M leaves in
+// 723 segments) groups first cut the per-tensor reduction by about a quarter.
+//
+// The kernels are written once over a node-hash policy: SHA-256 (32-byte nodes;
 // an interior node is two blocks) or SHA-384 (48-byte nodes; leaf and
 // interior nodes are one 128-byte block each).
 #include "hv_kernels.h"
@@ -124,7 +131,106 @@ __global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t*
     }
 }
 
+// The first launch of a large reduction (the host plans it for 2^18 entries or more):
+// lane g reduces group g of its segment -- entries [8t, min(8t + 8, c)) for
+// the segment's t-th group, c its entry count -- to one node in registers,
+// forming the leaf hashes first in leaf mode.  Groups start at multiples of
+// 8, so, as with tiles, the promotion of a short last group is the whole
+// tree's.  The entries go through a stack of perfect subtrees: entry j is
+// merged with the subtrees of the trailing one bits of j (a binary counter),
+// and a short group folds what is left, smallest subtree first, which is
+// RFC 6962's split at the largest power of two.  Every lane of a wave works
+// on the widest levels, with no barrier and no LDS; the loops stay rolled
+// (one leaf-hash and one node-hash site), and stack slots are picked with
+// selects so that the stack stays in registers.  An empty segment has one
+// group, the hash of no entries.
+template <class T>
+__global__ void __launch_bounds__(kThreads) merkle_group_kernel(const uint8_t* __restrict__ in,
+                                                                 uint8_t* __restrict__ out,
+                                                                 const uint64_t* __restrict__ in_off,
+                                                                 const uint64_t* __restrict__ grp_off, uint32_t n_seg,
+                                                                 uint64_t n_groups, int leaf_mode) {
+    constexpr int NW = T::kWords;
+    constexpr int NB = T::kBytes;
+    constexpr int L = kGroupLevels;
+    for (uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; g < n_groups;
+         g += (uint64_t)gridDim.x * blockDim.x) {
+        const uint32_t s = find_segment(grp_off, n_seg, g);
+        const uint64_t t = g - grp_off[s];
+        const uint64_t c = in_off[s + 1] - in_off[s];
+        const uint64_t first = t * kGroupNodes;
+        const uint32_t cnt =
+            c > first ? (uint32_t)(c - first < (uint64_t)kGroupNodes ? c - first : kGroupNodes) : 0u;
+        const uint8_t* base = in + NB * (in_off[s] + first);
+        uint32_t S[L][NW];  // S[l]: the perfect subtree of 2^l entries waiting for its right sibling
+        uint32_t X[NW];
+#pragma unroll
+        for (int l = 0; l < L; ++l)
+            for (int w = 0; w < NW; ++w) S[l][w] = 0;
+        if (cnt == 0) T::empty_hash(X);
+#pragma nounroll
+        for (uint32_t j = 0; j < cnt; ++j) {
+            uint32_t A[NW];
+            T::load(base + NB * j, A);
+            if (leaf_mode) T::leaf_hash(A, X); else for (int w = 0; w < NW; ++w) X[w] = A[w];
+            uint32_t l = 0;
+#pragma nounroll
+            while (l < (uint32_t)L && ((j >> l) & 1u)) {
+                uint32_t Y[NW], Z[NW];
+                for (int w = 0; w < NW; ++w) {
+                    uint32_t v = S[0][w];
+#pragma unroll
+                    for (int q = 1; q < L; ++q) v = l == (uint32_t)q ? S[q][w] : v;
+                    Y[w] = v;
+                }
+                T::node_hash(Y, X, Z);
+                for (int w = 0; w < NW; ++w) X[w] = Z[w];
+                ++l;
+            }
+#pragma unroll
+            for (int q = 0; q < L; ++q)
+                for (int w = 0; w < NW; ++w) S[q][w] = l == (uint32_t)q ? X[w] : S[q][w];
+        }
+        if (cnt > 0 && cnt < (uint32_t)kGroupNodes) {
+            bool have = false;
+#pragma nounroll
+            for (uint32_t l = 0; l < (uint32_t)L; ++l) {
+                if (!((cnt >> l) & 1u)) continue;
+                uint32_t Y[NW];
+                for (int w = 0; w < NW; ++w) {
+                    uint32_t v = S[0][w];
+#pragma unroll
+                    for (int q = 1; q < L; ++q) v = l == (uint32_t)q ? S[q][w] : v;
+                    Y[w] = v;
+                }
+                if (!have) {
+                    for (int w = 0; w < NW; ++w) X[w] = Y[w];
+                    have = true;
+                } else {
+                    uint32_t Z[NW];
+                    T::node_hash(Y, X, Z);
+                    for (int w = 0; w < NW; ++w) X[w] = Z[w];
+                }
+            }
+        }
+        T::store(out + NB * g, X);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_merkle_groups(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
+                                const uint64_t* grp_off, uint32_t n_seg, uint64_t n_groups, int leaf_mode,
+                                hipStream_t s) {
+    if (n_groups == 0) return hipSuccess;
+    const uint64_t blocks = (n_groups + kThreads - 1) / kThreads;
+    const unsigned grid = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));
+    if (alg == kAlgSha384)
+        merkle_group_kernel<Sha384Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, grp_off, n_seg, n_groups, leaf_mode);
+    else
+        merkle_group_kernel<Sha256Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, grp_off, n_seg, n_groups, leaf_mode);
+    return hipGetLastError();
+}
 
 hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
                                const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode,

@@ -140,6 +140,43 @@ def test_merkle_every_segment_size_up_to_600(alg):
     assert not bad, f"{alg}: roots differ for segment sizes {bad[:10]}"
 
 
+@pytest.mark.parametrize("alg", ["sha256", "sha384"])
+@pytest.mark.parametrize("big_first", [False, True])
+def test_merkle_group_launch_every_segment_size(alg, big_first):
+    # 2^18 entries or more start with a group launch (8 entries per lane,
+    # three levels in registers): every segment size 0..600 (every short last
+    # group, empty segments) in one call made large by a segment of 100,003
+    # entries, placed last or first; each root against the oracle and against
+    # the same segments reduced by the tile launches alone (a call under 2^18)
+    D = 32 if alg == "sha256" else 48
+    small = list(range(601))
+    sizes = [100_003] + small if big_first else small + [100_003]
+    n = sum(sizes)
+    assert n >= 1 << 18 and sum(small) < 1 << 18
+    entries = W.random_bytes(n * D, 260 + D + big_first, DEV).view(n, D)
+    seg = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    roots = hv.hv_merkle_reduce(entries, seg, alg=alg)
+    lo = 1 if big_first else 0
+    part = entries[int(seg[lo]):int(seg[lo + len(small)])]
+    part_roots = hv.hv_merkle_reduce(part.contiguous(), np.concatenate([[0], np.cumsum(small)]).astype(np.uint64),
+                                     alg=alg)
+    torch.cuda.synchronize()
+    host = entries.cpu().numpy()
+    want = [oracle.mth(host[int(seg[k]):int(seg[k + 1])], alg) for k in range(len(sizes))]
+    got = [bytes(r) for r in roots.cpu().numpy()]
+    bad = [sizes[k] for k in range(len(sizes)) if got[k] != want[k]]
+    assert not bad, f"{alg}: roots differ for segment sizes {bad[:10]}"
+    assert [bytes(r) for r in part_roots.cpu().numpy()] == want[lo:lo + len(small)]
+
+
+@pytest.mark.parametrize("n", [(1 << 18) - 1, 1 << 18, (1 << 18) + 1, (1 << 18) + 7, 3 * (1 << 18) + 5])
+def test_merkle_single_tree_around_the_group_threshold(n):
+    entries = W.random_bytes(n * 32, 270 + n % 97, DEV).view(n, 32)
+    root = hv.hv_merkle_reduce(entries, np.array([0, n], dtype=np.uint64))
+    torch.cuda.synchronize()
+    assert bytes(root.cpu().numpy().reshape(-1)) == oracle.mth(entries.cpu().numpy())
+
+
 def test_verify_and_compare():
     entries = W.random_bytes(5 * 32, 300, DEV).view(5, 32)
     root = hv.hv_merkle_reduce(entries, np.array([0, 5], dtype=np.uint64))
