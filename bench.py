@@ -126,7 +126,8 @@ def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
     """The oracle (plain C, threaded over chunks) on the first whole chunks of
     the first messages, about sample_bytes in all, one message at a time so
     that host memory stays bounded; only the oracle's work is timed.  Also
-    checks those digests against the GPU's."""
+    checks those digests against the GPU's, and the root of every message
+    sampled whole against the GPU's root of that message."""
     from oracle import oracle
 
     C = wl.chunk_bytes
@@ -134,6 +135,7 @@ def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
     threads = min(16, len(os.sched_getaffinity(0)))
     gpu = pipe.leaves
     left, nbytes, n_leaves, n_msgs, dt, ok = sample_bytes, 0, 0, 0, 0.0, True
+    roots_checked = roots_ok = 0
     if views is None and C == 0 and len(wl.msgs) > 1:
         # many whole messages packed in one buffer: copy the sampled range once
         # and hash it with the oracle's packed driver (one message at a time
@@ -149,6 +151,8 @@ def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
         oracle.mth(leaves, alg)
         dt = time.perf_counter() - t0
         ok = bool(np.array_equal(gpu[:k].cpu().numpy(), leaves))
+        if k == len(lens):  # every message sampled: the single tree's root too
+            roots_checked, roots_ok = 1, int(bytes(pipe.root.cpu().numpy().reshape(-1)) == oracle.mth(leaves, alg))
         nbytes, n_leaves, n_msgs, left = int(lens[:k].sum()), k, k, 0
         del host
     for m in range(len(wl.msgs)):
@@ -164,10 +168,14 @@ def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
         host = src.cpu().numpy()
         t0 = time.perf_counter()
         leaves = oracle.leaf_digests_mt([host], C, threads, alg)
-        oracle.mth(leaves, alg)
+        root = oracle.mth(leaves, alg)
         dt += time.perf_counter() - t0
         first = int(pipe.seg[m])
         ok &= bool(np.array_equal(gpu[first:first + len(leaves)].cpu().numpy(), leaves))
+        if n == L and (wl.manifest or len(wl.msgs) == 1):  # the whole message was sampled: its root too
+            roots_checked += 1
+            gpu_root = pipe.roots[m] if wl.manifest else pipe.root.reshape(-1)
+            roots_ok += int(bytes(gpu_root.cpu().numpy()) == root)
         nbytes += n
         n_leaves += len(leaves)
         n_msgs += 1
@@ -188,6 +196,8 @@ def cpu_baseline(wl, pipe, sample_bytes, alg="sha256"):
                   f"message at a time; oracle chunk digests on {threads} threads + the Merkle root over them; "
                   f"device-to-host copies not timed",
         "seconds": round(dt, 3), "matches_gpu_digests": ok,
+        # messages sampled whole: their roots (the oracle's recursive tree) against the GPU's
+        "roots_compared": roots_checked, "matches_gpu_roots": roots_ok == roots_checked,
     }
 
 
@@ -629,11 +639,13 @@ def main():
     for _ in range(args.warmup):
         assert oneshot_step()
     hv.set_kernel_timing(True)
-    kernel_ms = []
+    kernel_ms, step_ms = [], []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        ok = oneshot_step()
+        ts = time.perf_counter()
+        ok = oneshot_step()  # synchronous: it ends with the verdict on the host
+        step_ms.append((time.perf_counter() - ts) * 1e3)
         kernel_ms.append(hv.leaf_kernel_ms())
         assert ok
     torch.cuda.synchronize()
@@ -673,13 +685,19 @@ def main():
     total = pipe.total_bytes
     value = total / (ms_step / 1e3) / 1e9
     k_ms = float(np.mean(kernel_ms))
+    med = float(np.median(step_ms))
+    step_stats = {"median": round(med, 3), "min": round(min(step_ms), 3), "max": round(max(step_ms), 3),
+                  "spread_pct": round((max(step_ms) - min(step_ms)) / med * 100, 2),
+                  "median_GBps": round(total / (med / 1e3) / 1e9, 2),
+                  "leaf_kernel_median_ms": round(float(np.median(kernel_ms)), 3)}
     blocks = sha_blocks(wl.msgs.lens, wl.chunk_bytes, alg)
     achieved = blocks * ops_per_block / (k_ms / 1e3) / 1e12
     ran = hv.leaf_kernel_for(pipe.n_leaves)  # the leaf kernel the timed passes ran
     if ran != "one-wave":
         leaf_kernel = f"{alg}_split_kernel"
-    log(f"{args.steps} steps: {ms_step:.2f} ms/step, {value:.1f} GB/s; leaf kernel {k_ms:.2f} ms avg "
-        f"({total / k_ms / 1e6:.1f} GB/s, {achieved:.2f} TOP/s); prepared pass {prepared_ms:.2f} ms/step")
+    log(f"{args.steps} steps: {ms_step:.2f} ms/step, {value:.1f} GB/s (median step {med:.2f} ms, spread "
+        f"{step_stats['spread_pct']:.2f}%); leaf kernel {k_ms:.2f} ms avg ({total / k_ms / 1e6:.1f} GB/s, "
+        f"{achieved:.2f} TOP/s); prepared pass {prepared_ms:.2f} ms/step")
 
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -692,6 +710,7 @@ def main():
             "step": "one-shot calls: descriptor upload, leaf scheduling, leaf hashes, per-tensor roots, manifest, "
                     "root compare" if wl.manifest else
                     "one-shot calls: descriptor upload, leaf scheduling, leaf hashes, one tree, root compare",
+            "step_ms": step_stats,
             "leaf_kernel": args.leaf_kernel, "leaf_kernel_ran": ran,
             "prepared_ms_per_step": round(prepared_ms, 3),
             "prepared_GBps": round(pipe.total_bytes / (prepared_ms / 1e3) / 1e9, 2),

@@ -32,9 +32,11 @@
  *     device needs them, before the call returns, whatever memory they are in
  *     (pageable or pinned); such a call returns once `stream` has reached and
  *     finished its uploads.
- *   - All argument checks happen before any work is queued; on a non-OK
- *     status nothing was launched (except HV_ERR_HIP, which reports a failed
- *     launch or copy) and hv_last_error() describes the problem.
+ *   - All argument checks happen before any kernel is queued; on a non-OK
+ *     status no kernel was launched (except HV_ERR_HIP, which reports a failed
+ *     launch or copy) and hv_last_error() describes the problem.  (A large
+ *     descriptor table may already have been copied into the workspace,
+ *     which is scratch: hv_hash_chunks starts that upload while it checks.)
  *   - A root mismatch is not an error: hv_verify_root returns HV_OK, *match=0.
  *   - No global state except a thread-local error string (and the static
  *     scratch of hv_hash_chunks_noalloc).  Concurrent calls on different

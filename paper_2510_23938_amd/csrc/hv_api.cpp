@@ -9,6 +9,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <thread>
 #include <vector>
 
 #include "hv_host.h"
@@ -43,34 +44,122 @@ HashLayout hash_layout(void* ws, uint32_t n_msgs, uint64_t n_leaves) {
     return L;
 }
 
-// Leaf counts of a message list; fills seg_offsets when given.
+namespace {
+
+// Why a message is refused (kNone: it is not).
+enum BadMsg : int { kNone = 0, kNullData, kWraps, kChunkTooLarge, kCountOverflow };
+
+// Validates messages [lo, hi) and counts their leaves (and full chunks); with
+// seg_offsets, writes seg_offsets[m + 1] = base + leaves of messages lo..m.
+// Stops at the first refused message: *bad_at and the returned reason.
+BadMsg scan_messages(const hv_msg* msgs, uint32_t lo, uint32_t hi, uint64_t C, uint64_t base,
+                     uint64_t* seg_offsets, uint64_t* leaves_out, uint64_t* full_out, uint32_t* bad_at) {
+    uint64_t total = 0, full = 0;
+    for (uint32_t m = lo; m < hi; ++m) {
+        const uint64_t len = msgs[m].nbytes;
+        BadMsg why = kNone;
+        if (len > 0 && msgs[m].data == nullptr) why = kNullData;
+        else if ((uintptr_t)msgs[m].data + len < (uintptr_t)msgs[m].data) why = kWraps;
+        else if ((C == 0 || len < C ? len : C) > kMaxChunkBytes) why = kChunkTooLarge;
+        uint64_t leaves = 0;
+        if (why == kNone) {
+            if (C == 0) {
+                leaves = 1;
+            } else {
+                leaves = len / C + (len % C != 0);
+                full += len / C;
+            }
+            if (total + leaves < total || base + total + leaves < base) why = kCountOverflow;
+        }
+        if (why != kNone) {
+            *bad_at = m;
+            return why;
+        }
+        total += leaves;
+        if (seg_offsets) seg_offsets[m + 1] = base + total;
+    }
+    *leaves_out = total;
+    *full_out = full;
+    return kNone;
+}
+
+hv_status refuse(const hv_msg* msgs, uint32_t m, uint64_t C, BadMsg why) {
+    switch (why) {
+        case kNullData:
+            return fail(HV_ERR_INVALID_ARG, "message %u has NULL data and %llu bytes", m,
+                        (unsigned long long)msgs[m].nbytes);
+        case kWraps:
+            return fail(HV_ERR_INVALID_ARG, "message %u wraps the address space", m);
+        case kChunkTooLarge: {
+            const uint64_t len = msgs[m].nbytes;
+            return fail(HV_ERR_INVALID_ARG, "message %u: a chunk of %llu bytes exceeds the %llu-byte limit", m,
+                        (unsigned long long)(C == 0 || len < C ? len : C), (unsigned long long)kMaxChunkBytes);
+        }
+        default:
+            return fail(HV_ERR_INVALID_ARG, "leaf count overflows");
+    }
+}
+
+// Message tables at least this long are scanned by several host threads.
+constexpr uint32_t kParallelScanMin = 1u << 16;
+
+}  // namespace
+
+// Leaf counts of a message list; fills seg_offsets when given.  Large tables
+// are split over host threads; whatever the split, the error reported is the
+// one of the lowest refused message, as a single pass would report it.
 hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_offsets, uint64_t* n_leaves,
                  uint64_t* n_full) {
     if (n_msgs > 0 && msgs == nullptr) return fail(HV_ERR_INVALID_ARG, "msgs is NULL with n_msgs = %u", n_msgs);
     if (C % 64 != 0) return fail(HV_ERR_INVALID_ARG, "chunk_bytes = %llu is not 0 or a multiple of 64",
                                  (unsigned long long)C);
-    uint64_t total = 0, full = 0;
     if (seg_offsets) seg_offsets[0] = 0;
-    for (uint32_t m = 0; m < n_msgs; ++m) {
-        const uint64_t len = msgs[m].nbytes;
-        if (len > 0 && msgs[m].data == nullptr)
-            return fail(HV_ERR_INVALID_ARG, "message %u has NULL data and %llu bytes", m, (unsigned long long)len);
-        if ((uintptr_t)msgs[m].data + len < (uintptr_t)msgs[m].data)
-            return fail(HV_ERR_INVALID_ARG, "message %u wraps the address space", m);
-        const uint64_t longest = C == 0 || len < C ? len : C;
-        if (longest > kMaxChunkBytes)
-            return fail(HV_ERR_INVALID_ARG, "message %u: a chunk of %llu bytes exceeds the %llu-byte limit", m,
-                        (unsigned long long)longest, (unsigned long long)kMaxChunkBytes);
-        uint64_t leaves;
-        if (C == 0) {
-            leaves = 1;
-        } else {
-            leaves = len / C + (len % C != 0);
-            full += len / C;
+    unsigned T = 1;
+    if (n_msgs >= kParallelScanMin) {
+        const unsigned hw = std::thread::hardware_concurrency();
+        T = hw == 0 ? 1 : (hw < 16 ? hw : 16);
+    }
+    uint64_t total = 0, full = 0;
+    if (T <= 1) {
+        uint32_t bad = 0;
+        const BadMsg why = scan_messages(msgs, 0, n_msgs, C, 0, seg_offsets, &total, &full, &bad);
+        if (why != kNone) return refuse(msgs, bad, C, why);
+    } else {
+        // pass 1: counts per part (no offsets); pass 2: offsets from each part's base
+        std::vector<uint64_t> leaves(T, 0), fulls(T, 0);
+        std::vector<uint32_t> bad(T, 0);
+        std::vector<BadMsg> why(T, kNone);
+        auto part = [&](unsigned t) { return (uint32_t)((uint64_t)n_msgs * t / T); };
+        {
+            std::vector<std::thread> pool;
+            for (unsigned t = 1; t < T; ++t)
+                pool.emplace_back([&, t] {
+                    why[t] = scan_messages(msgs, part(t), part(t + 1), C, 0, nullptr, &leaves[t], &fulls[t], &bad[t]);
+                });
+            why[0] = scan_messages(msgs, part(0), part(1), C, 0, nullptr, &leaves[0], &fulls[0], &bad[0]);
+            for (auto& th : pool) th.join();
         }
-        if (total + leaves < total) return fail(HV_ERR_INVALID_ARG, "leaf count overflows");
-        total += leaves;
-        if (seg_offsets) seg_offsets[m + 1] = total;
+        std::vector<uint64_t> base(T, 0);
+        for (unsigned t = 0; t < T; ++t) {
+            if (why[t] != kNone) return refuse(msgs, bad[t], C, why[t]);
+            if (total + leaves[t] < total) return fail(HV_ERR_INVALID_ARG, "leaf count overflows");
+            base[t] = total;
+            total += leaves[t];
+            full += fulls[t];
+        }
+        if (seg_offsets) {
+            std::vector<std::thread> pool;
+            uint64_t unused_leaves, unused_full;
+            uint32_t unused_bad;
+            for (unsigned t = 1; t < T; ++t)
+                pool.emplace_back([&, t] {
+                    uint64_t l, f;
+                    uint32_t b;
+                    (void)scan_messages(msgs, part(t), part(t + 1), C, base[t], seg_offsets, &l, &f, &b);
+                });
+            (void)scan_messages(msgs, part(0), part(1), C, 0, seg_offsets, &unused_leaves, &unused_full, &unused_bad);
+            for (auto& th : pool) th.join();
+        }
     }
     *n_leaves = total;
     if (n_full) *n_full = full;
@@ -192,33 +281,75 @@ hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t 
 
 namespace {
 
+// A descriptor upload started before the host validates the table, so that
+// the DMA runs under the validation.  The host array is consumed once wait()
+// returns; every path out of a call that started one goes through wait().
+thread_local hipEvent_t g_upload_event = nullptr;  // one per thread, kept for the thread's life
+constexpr uint32_t kEarlyUploadMin = 4096;           // smaller tables upload in a few microseconds
+
+struct Upload {
+    bool pending = false;
+    hv_status wait(hv_status st) {
+        if (!pending) return st;
+        pending = false;
+        const hipError_t e = hipEventSynchronize(g_upload_event);
+        return st == HV_OK && e != hipSuccess ? hip_fail(e, "descriptor upload") : st;
+    }
+};
+
 // Validation plus the scheduling kernels shared by hv_hash_chunks and
-// hv_leaf_schedule.  On HV_OK the leaf table is queued into L.desc.
+// hv_leaf_schedule.  On HV_OK the leaf table is queued into L.desc.  With
+// early_upload, a large descriptor table is copied asynchronously while the
+// host validates it; the caller then queues its own kernels and calls
+// up->wait() before returning (on an error, schedule has already waited).
 hv_status schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, bool need_out, const void* out,
-                   void* workspace, size_t workspace_bytes, hipStream_t stream, HashLayout* L_out,
-                   uint64_t* n_leaves_out) {
+                   void* workspace, size_t workspace_bytes, bool early_upload, Upload* up, hipStream_t stream,
+                   HashLayout* L_out, uint64_t* n_leaves_out) {
+    static_assert(sizeof(hv_msg) == sizeof(hv::MsgDesc), "hv_msg layout");
+    // The descriptors are the workspace's first region; start their copy when
+    // the workspace can hold them (it is scratch, whatever the checks find).
+    if (early_upload && n_msgs >= kEarlyUploadMin && msgs != nullptr && chunk_bytes % 64 == 0 &&
+        workspace != nullptr && (uintptr_t)workspace % kAlign == 0 &&
+        workspace_bytes >= round_up(sizeof(hv_msg) * (size_t)n_msgs)) {
+        hipError_t e = hipSuccess;
+        if (g_upload_event == nullptr) e = hipEventCreateWithFlags(&g_upload_event, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipMemcpyAsync(workspace, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
+        if (e == hipSuccess) {
+            up->pending = true;
+            e = hipEventRecord(g_upload_event, stream);
+            if (e != hipSuccess) {
+                // no event to wait on: wait for the stream itself before the host array is released
+                up->pending = false;
+                (void)hipStreamSynchronize(stream);
+            }
+        }
+        if (e != hipSuccess) return hip_fail(e, "descriptor upload");
+    }
     uint64_t n_leaves = 0, n_full = 0;
     hv_status st = layout(msgs, n_msgs, chunk_bytes, nullptr, &n_leaves, &n_full);
-    if (st != HV_OK) return st;
-    if (n_leaves > kMaxLeaves) return fail(HV_ERR_INVALID_ARG, "%llu leaves exceed the per-call limit",
-                                           (unsigned long long)n_leaves);
-    if (need_out && n_leaves > 0 && out == nullptr) return fail(HV_ERR_INVALID_ARG, "leaf_digests is NULL");
-    if (need_out && (uintptr_t)out % 16 != 0) return fail(HV_ERR_INVALID_ARG, "leaf_digests is not 16-byte aligned");
-    if (!need_out && n_leaves > 0 && out == nullptr) return fail(HV_ERR_INVALID_ARG, "table is NULL");
+    if (st != HV_OK) return up->wait(st);
+    if (n_leaves > kMaxLeaves)
+        return up->wait(fail(HV_ERR_INVALID_ARG, "%llu leaves exceed the per-call limit", (unsigned long long)n_leaves));
+    if (need_out && n_leaves > 0 && out == nullptr) return up->wait(fail(HV_ERR_INVALID_ARG, "leaf_digests is NULL"));
+    if (need_out && (uintptr_t)out % 16 != 0)
+        return up->wait(fail(HV_ERR_INVALID_ARG, "leaf_digests is not 16-byte aligned"));
+    if (!need_out && n_leaves > 0 && out == nullptr) return up->wait(fail(HV_ERR_INVALID_ARG, "table is NULL"));
     const HashLayout need = hash_layout(nullptr, n_msgs, n_leaves);
     if (workspace == nullptr || workspace_bytes < need.bytes)
-        return fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu%s", need.bytes, workspace_bytes,
-                    workspace ? "" : " (NULL)");
-    if ((uintptr_t)workspace % kAlign != 0) return fail(HV_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+        return up->wait(fail(HV_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu%s", need.bytes, workspace_bytes,
+                             workspace ? "" : " (NULL)"));
+    if ((uintptr_t)workspace % kAlign != 0) return up->wait(fail(HV_ERR_WORKSPACE, "workspace is not 256-byte aligned"));
     *n_leaves_out = n_leaves;
     *L_out = hash_layout(workspace, n_msgs, n_leaves);
     if (n_msgs == 0) return HV_OK;
 
     const HashLayout& L = *L_out;
-    static_assert(sizeof(hv_msg) == sizeof(hv::MsgDesc), "hv_msg layout");
-    hipError_t e = hipMemcpyWithStream(L.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
-    if (e != hipSuccess) return hip_fail(e, "descriptor upload");
-    return hvh::queue_schedule(L.msgs, n_msgs, chunk_bytes, n_full, n_leaves, L, stream);
+    if (!up->pending) {
+        const hipError_t e = hipMemcpyWithStream(L.msgs, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
+        if (e != hipSuccess) return hip_fail(e, "descriptor upload");
+    }
+    st = hvh::queue_schedule(L.msgs, n_msgs, chunk_bytes, n_full, n_leaves, L, stream);
+    return st == HV_OK ? st : up->wait(st);
 }
 
 }  // namespace
@@ -226,7 +357,7 @@ hv_status schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, bo
 namespace hvh {
 
 hv_status hash_chunks_into(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
-                           uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, bool timed,
+                           uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, bool events,
                            hipStream_t stream) {
     if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
     if (alg == HV_SHA384 && chunk_bytes % 128 != 0)
@@ -234,15 +365,18 @@ hv_status hash_chunks_into(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint
                     (unsigned long long)chunk_bytes);
     HashLayout L;
     uint64_t n_leaves = 0;
-    hv_status st = schedule(msgs, n_msgs, chunk_bytes, true, leaf_digests, workspace, workspace_bytes, stream, &L,
-                            &n_leaves);
-    if (st != HV_OK || n_leaves == 0) return st;
+    // with events, the descriptor upload overlaps the validation
+    Upload up;
+    hv_status st = schedule(msgs, n_msgs, chunk_bytes, true, leaf_digests, workspace, workspace_bytes, events, &up,
+                            stream, &L, &n_leaves);
+    if (st != HV_OK) return st;
+    if (n_leaves == 0) return up.wait(HV_OK);
 
-    if (timed && (st = leaf_timing_start(stream)) != HV_OK) return st;
+    if (events && (st = leaf_timing_start(stream)) != HV_OK) return up.wait(st);
     const hipError_t e = alg == HV_SHA384 ? hv::launch_sha384_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream)
                                           : hv::launch_sha256_auto(L.desc, n_leaves, n_leaves, leaf_digests, stream);
-    if (e != hipSuccess) return hip_fail(e, "leaf kernel");
-    return timed ? leaf_timing_stop(stream) : HV_OK;
+    if (e != hipSuccess) return up.wait(hip_fail(e, "leaf kernel"));
+    return up.wait(events ? leaf_timing_stop(stream) : HV_OK);
 }
 
 }  // namespace hvh
@@ -279,9 +413,10 @@ hv_status hv_leaf_schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_b
                            void* workspace, size_t workspace_bytes, hipStream_t stream) {
     HashLayout L;
     uint64_t n_leaves = 0;
-    hv_status st = schedule(msgs, n_msgs, chunk_bytes, false, table, workspace, workspace_bytes, stream, &L,
-                            &n_leaves);
-    if (st != HV_OK || n_leaves == 0) return st;
+    Upload up;
+    hv_status st = schedule(msgs, n_msgs, chunk_bytes, false, table, workspace, workspace_bytes, true, &up, stream,
+                            &L, &n_leaves);
+    if ((st = up.wait(st)) != HV_OK || n_leaves == 0) return st;
     static_assert(sizeof(hv::LeafDesc) == 3 * sizeof(uint64_t), "leaf table layout");
     hipError_t e = hipMemcpyAsync(table, L.desc, n_leaves * sizeof(hv::LeafDesc), hipMemcpyDeviceToHost, stream);
     if (e != hipSuccess) return hip_fail(e, "table copy");

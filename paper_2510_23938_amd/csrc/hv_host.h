@@ -57,10 +57,12 @@ hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_
                  uint64_t* n_full);
 
 // The body of hv_hash_chunks_alg over a given workspace (validation, descriptor
-// upload, scheduling, leaf kernel); `timed` records the leaf-kernel events of
-// hv_set_kernel_timing when that is on.
+// upload, scheduling, leaf kernel).  With `events` the call may create and use
+// HIP events: a large descriptor table is then uploaded asynchronously while
+// the host validates it, and the leaf kernel is timed when
+// hv_set_kernel_timing is on; without, it creates no runtime object.
 hv_status hash_chunks_into(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes,
-                           uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, bool timed,
+                           uint8_t* leaf_digests, void* workspace, size_t workspace_bytes, bool events,
                            hipStream_t stream);
 
 // Scheduling kernels over device-resident descriptors into L (leaf table in L.desc).

@@ -76,7 +76,8 @@ extern "C" hv_status hv_hash_chunks_noalloc(hv_alg alg, const hv_msg* msgs, uint
                     n_msgs, (unsigned long long)n_leaves, need, (size_t)HV_NOALLOC_SCRATCH_BYTES);
     void* ws = nullptr;
     if ((st = scratch_of(stream, &ws)) != HV_OK) return st;
-    // No timing events here: creating them is an allocation of the runtime's.
+    // No events here (no timing, a blocking descriptor upload): creating them
+    // would allocate runtime objects.
     return hash_chunks_into(alg, msgs, n_msgs, chunk_bytes, leaf_digests, ws, HV_NOALLOC_SCRATCH_BYTES, false,
                             stream);
 }

@@ -147,13 +147,24 @@ __device__ __forceinline__ bool tail_of(const MsgDesc& msg, uint64_t C, uint64_t
     return *len != 0;
 }
 
+// Tail counts per sort class.  Each workgroup counts its messages' classes in
+// LDS and adds its non-zero counts to the global histogram: one global atomic
+// per class a workgroup meets, not one per message (10^6 messages fall into
+// about a thousand classes, and per-message atomics on so few addresses
+// serialise).
 __global__ void __launch_bounds__(kThreads) tail_hist_kernel(const MsgDesc* __restrict__ msgs, uint32_t n, uint64_t C,
                                                              uint64_t* __restrict__ hist) {
+    __shared__ uint32_t local[kSortBuckets];
+    for (int k = threadIdx.x; k < kSortBuckets; k += kThreads) local[k] = 0;
+    __syncthreads();
     for (size_t m = (size_t)blockIdx.x * kThreads + threadIdx.x; m < n; m += (size_t)gridDim.x * kThreads) {
         uint64_t start, len;
         const MsgDesc msg = msgs[m];
-        if (tail_of(msg, C, &start, &len)) atomicAdd((unsigned long long*)&hist[block_class(sha_blocks(len))], 1ull);
+        if (tail_of(msg, C, &start, &len)) atomicAdd(&local[block_class(sha_blocks(len))], 1u);
     }
+    __syncthreads();
+    for (int k = threadIdx.x; k < kSortBuckets; k += kThreads)
+        if (local[k] != 0) atomicAdd((unsigned long long*)&hist[k], (unsigned long long)local[k]);
 }
 
 // hist[k] <- first table slot of class k, largest class first (one block).
@@ -173,15 +184,37 @@ __global__ void __launch_bounds__(kThreads) tail_cursor_kernel(uint64_t* __restr
     }
 }
 
+// Tail leaves into their class ranges.  A workgroup counts its messages per
+// class in LDS, reserves one contiguous run of slots per class it meets with
+// a single global atomic on that class's cursor, then gives each message the
+// next slot of its class's run by an LDS atomic.  Slots of one class are
+// therefore handed out in no fixed order, which is fine: leaves of one class
+// have (about) the same block count, and the order never changes a digest.
 __global__ void __launch_bounds__(kThreads) tail_scatter_kernel(const MsgDesc* __restrict__ msgs,
                                                                 const Pair* __restrict__ off, uint32_t n, uint64_t C,
                                                                 uint64_t* __restrict__ cursor,
                                                                 LeafDesc* __restrict__ desc) {
+    __shared__ uint32_t local[kSortBuckets];  // this workgroup's count per class, then the next rank
+    __shared__ uint64_t run[kSortBuckets];    // first slot of this workgroup's run in each class
+    for (int k = threadIdx.x; k < kSortBuckets; k += kThreads) local[k] = 0;
+    __syncthreads();
+    for (size_t m = (size_t)blockIdx.x * kThreads + threadIdx.x; m < n; m += (size_t)gridDim.x * kThreads) {
+        uint64_t start, len;
+        const MsgDesc msg = msgs[m];
+        if (tail_of(msg, C, &start, &len)) atomicAdd(&local[block_class(sha_blocks(len))], 1u);
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < kSortBuckets; k += kThreads) {
+        if (local[k] != 0) run[k] = atomicAdd((unsigned long long*)&cursor[k], (unsigned long long)local[k]);
+        local[k] = 0;
+    }
+    __syncthreads();
     for (size_t m = (size_t)blockIdx.x * kThreads + threadIdx.x; m < n; m += (size_t)gridDim.x * kThreads) {
         uint64_t start, len;
         const MsgDesc msg = msgs[m];
         if (!tail_of(msg, C, &start, &len)) continue;
-        const uint64_t slot = atomicAdd((unsigned long long*)&cursor[block_class(sha_blocks(len))], 1ull);
+        const uint32_t k = block_class(sha_blocks(len));
+        const uint64_t slot = run[k] + atomicAdd(&local[k], 1u);
         const Pair o = off[m];
         LeafDesc d;
         d.src = msg.data + start;
@@ -305,12 +338,20 @@ hipError_t launch_sched_range(const MsgDesc* msgs, const Pair* off, uint32_t n, 
     return hipGetLastError();
 }
 
+// Workgroups of the privatised tail kernels: enough to spread the messages,
+// few enough that each covers many messages (its class counts are summed
+// once per workgroup).
+unsigned tail_grid(uint64_t n) {
+    const uint64_t blocks = (n + kThreads - 1) / kThreads;
+    return (unsigned)(blocks == 0 ? 1 : (blocks < 512 ? blocks : 512));
+}
+
 hipError_t launch_sched_tails(const MsgDesc* msgs, const Pair* off, uint32_t n, uint64_t C, uint64_t n_full,
                               uint64_t* hist, LeafDesc* desc, hipStream_t s) {
     fill_u64_kernel<<<grid_for(kSortBuckets), kThreads, 0, s>>>(hist, kSortBuckets, 0);
-    tail_hist_kernel<<<grid_for(n), kThreads, 0, s>>>(msgs, n, C, hist);
+    tail_hist_kernel<<<tail_grid(n), kThreads, 0, s>>>(msgs, n, C, hist);
     tail_cursor_kernel<<<1, kThreads, 0, s>>>(hist, n_full);
-    tail_scatter_kernel<<<grid_for(n), kThreads, 0, s>>>(msgs, off, n, C, hist, desc);
+    tail_scatter_kernel<<<tail_grid(n), kThreads, 0, s>>>(msgs, off, n, C, hist, desc);
     return hipGetLastError();
 }
 

@@ -305,16 +305,48 @@ def _merkle_ws_bytes(alg: str, n_nodes: int, n_seg: int) -> int:
     return lib.hv_merkle_workspace_bytes_alg(code, n_nodes, n_seg)
 
 
+class _TableCache:
+    """The descriptor table and leaf layout of the last message set, kept while
+    that set's ``ptrs`` and ``lens`` are the same read-only numpy arrays: both are
+    pure functions of those arrays and the chunk size, so they are rebuilt only
+    when the set changes.  The library still validates and uploads the table on
+    every call.  Writable arrays are never cached."""
+
+    def __init__(self, pinned: bool = True):
+        self.key = None
+        self.pinned = pinned  # pinned tables upload by DMA
+
+    def lookup(self, ptrs, lens, chunk_bytes: int):
+        if not (isinstance(ptrs, np.ndarray) and isinstance(lens, np.ndarray)) or \
+                ptrs.flags.writeable or lens.flags.writeable:
+            return None
+        if self.key is not None and self.key[0] is ptrs and self.key[1] is lens and self.key[2] == chunk_bytes:
+            return self.table
+        host = HostBuffer(pinned=self.pinned)  # owned by this entry
+        arr = _msg_array(ptrs, lens, host)
+        seg, n_leaves = _layout_of(arr, chunk_bytes)
+        seg.flags.writeable = False
+        self.key = (ptrs, lens, chunk_bytes)  # the references keep the arrays (and so their ids) alive
+        self.host = host
+        self.table = (arr, seg, n_leaves)
+        return self.table
+
+
 def hv_hash_chunks(msgs, chunk_bytes: int, device="cuda", workspace: Workspace | None = None, out=None,
-                   alg: str = "sha256", host: HostBuffer | None = None, seg_host: HostBuffer | None = None):
+                   alg: str = "sha256", host: HostBuffer | None = None, seg_host: HostBuffer | None = None,
+                   table=None):
     """Leaf digests of ``msgs`` (tensors, a (ptrs, lens) pair, or an object with
     ``ptrs``/``lens``): ([n_leaves, D] uint8 device tensor, seg_offsets), D the digest size.
     ``host`` holds the descriptor table; with ``seg_host`` the returned seg_offsets
-    live in that buffer, valid until its next use."""
+    live in that buffer, valid until its next use.  ``table``: the (descriptor
+    table, seg_offsets, n_leaves) of ``msgs`` when the caller already has them."""
     _, D = _alg(alg)
-    ptrs, lens = _ptr_len(msgs)
-    arr = _msg_array(ptrs, lens, host)
-    seg, n_leaves = _layout_of(arr, chunk_bytes, seg_host)
+    if table is not None:
+        arr, seg, n_leaves = table
+    else:
+        ptrs, lens = _ptr_len(msgs)
+        arr = _msg_array(ptrs, lens, host)
+        seg, n_leaves = _layout_of(arr, chunk_bytes, seg_host)
     n = len(arr)
     dev = torch.device(device)
     if out is None:
@@ -581,10 +613,13 @@ class Verifier:
         self.ws_verify = Workspace(self.device)
         self.host_msgs = HostBuffer(pinned=True)    # descriptor tables, uploaded by DMA
         self.host_seg = HostBuffer(pinned=False)    # offsets used only inside one call
+        self.tables = _TableCache()                 # for message sets given as read-only arrays
 
     def _leaves(self, msgs, chunk_bytes: int, keep_seg: bool):
-        return hv_hash_chunks(msgs, chunk_bytes, self.device, self.ws_hash, alg=self.alg, host=self.host_msgs,
-                              seg_host=None if keep_seg else self.host_seg)
+        ptrs, lens = _ptr_len(msgs)
+        return hv_hash_chunks((ptrs, lens), chunk_bytes, self.device, self.ws_hash, alg=self.alg, host=self.host_msgs,
+                              seg_host=None if keep_seg else self.host_seg,
+                              table=self.tables.lookup(ptrs, lens, chunk_bytes))
 
     def leaf_digests(self, msgs, chunk_bytes: int):
         return self._leaves(msgs, chunk_bytes, True)

@@ -444,3 +444,60 @@ def test_noalloc_refuses_what_its_static_scratch_cannot_hold():
     assert hv.lib.hv_hash_chunks_noalloc(hv.HV_SHA256, p, 2, 64, 0x1008, None) == hv.HV_ERR_INVALID_ARG
     assert b"16-byte aligned" in hv.lib.hv_last_error()
     assert hv.lib.hv_hash_chunks_noalloc(hv.HV_SHA256, None, 2, 64, 0x1000, None) == hv.HV_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("C", [0, 64, 4096])
+def test_large_message_tables_are_laid_out_as_one_pass_would(C):
+    # tables of 2^16 messages or more are validated and counted by several host
+    # threads: the offsets and counts are those of the plain chunk-count rule
+    n = 1_000_003
+    lens = np.random.default_rng(41).integers(0, 70000, n).astype(np.uint64)
+    ptrs = np.uint64(1 << 40) + np.arange(n, dtype=np.uint64) * np.uint64(1 << 17)
+    seg, total = hv.hv_leaf_layout(ptrs, lens, C)
+    per = np.ones(n, dtype=np.uint64) if C == 0 else (lens + np.uint64(C - 1)) // np.uint64(C)
+    assert total == int(per.sum())
+    assert seg[0] == 0 and np.array_equal(seg[1:], np.cumsum(per))
+    assert hv.lib.hv_hash_workspace_bytes(n, total) > 0
+
+
+def test_large_message_tables_report_the_lowest_refused_message():
+    n = 300_000
+    lens = np.full(n, 1000, dtype=np.uint64)
+    ptrs = np.uint64(1 << 40) + np.arange(n, dtype=np.uint64) * np.uint64(4096)
+    for bad in ([299_999], [150_000, 7], [7, 150_000], [0], [250_000, 40_000, 260_000]):
+        p = ptrs.copy()
+        p[bad] = 0  # NULL data with 1000 bytes
+        with pytest.raises(hv.HVError) as e:
+            hv.hv_leaf_layout(p, lens, 64)
+        assert f"message {min(bad)} has NULL data" in str(e.value), bad
+    # a chunk over the size limit, and an address range that wraps, in other parts of the table
+    l2 = lens.copy()
+    l2[200_000] = (1 << 37) + 64
+    with pytest.raises(hv.HVError) as e:
+        hv.hv_leaf_layout(ptrs, l2, 0)
+    assert "message 200000: a chunk of" in str(e.value)
+    p = ptrs.copy()
+    p[123_456] = np.uint64((1 << 64) - 100)
+    with pytest.raises(hv.HVError) as e:
+        hv.hv_leaf_layout(p, lens, 64)
+    assert "message 123456 wraps" in str(e.value)
+
+
+def test_descriptor_table_cache_only_for_read_only_arrays():
+    cache = hv._TableCache(pinned=False)  # (pinned host memory needs a GPU)
+    lens = np.array([0, 100, 5000, 70000], dtype=np.uint64)
+    ptrs = np.array([0, 0x10000, 0x20000, 0x40000], dtype=np.uint64)
+    assert cache.lookup(ptrs, lens, 4096) is None  # writable: never cached
+    ptrs.flags.writeable = False
+    lens.flags.writeable = False
+    arr, seg, n = cache.lookup(ptrs, lens, 4096)
+    assert n == 0 + 1 + 2 + 18 and list(seg) == [0, 0, 1, 3, 21]
+    assert list(arr[:, 0]) == list(ptrs) and list(arr[:, 1]) == list(lens)
+    assert cache.lookup(ptrs, lens, 4096)[0] is arr  # same set: the same table
+    arr2, seg2, n2 = cache.lookup(ptrs, lens, 0)     # another chunk size: rebuilt
+    assert n2 == 4 and list(seg2) == [0, 1, 2, 3, 4]
+    with pytest.raises(ValueError):
+        seg2[0] = 5  # the cached offsets are read-only too
+    other = lens.copy()
+    other.flags.writeable = False
+    assert cache.lookup(ptrs, other, 0)[0] is not arr2  # an equal but different array object: rebuilt

@@ -81,3 +81,66 @@ def test_plan_init_reads_a_pinned_table_during_the_call(buffers):
     assert np.array_equal(leaves.cpu().numpy(), want)
     counts = [oracle.chunk_count(L, C) for L in LENS]
     assert bytes(root.cpu().numpy().reshape(-1)) == oracle.mth(oracle.seg_roots_from_leaves(want, counts))
+
+
+N_BIG = 6000  # a table of at least 4096 messages is uploaded while the host checks it
+
+
+@pytest.fixture
+def big_tables():
+    lens = np.random.default_rng(1500).integers(0, 3000, N_BIG).astype(np.uint64)
+    starts = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.uint64)
+    total = int(lens.sum())
+    A = W.random_bytes(total + 1, 1501, DEV)
+    B = W.random_bytes(total + 1, 1502, DEV)
+    torch.cuda.synchronize()
+    pinned = torch.empty((N_BIG, 2), dtype=torch.int64, pin_memory=True)
+    table = pinned.numpy().view(np.uint64)
+
+    def point(buf):
+        table[:, 0] = np.uint64(buf.data_ptr()) + starts
+        table[:, 1] = lens
+
+    host = A.cpu().numpy()
+    want = oracle.leaf_digests_mt([host[int(o):int(o) + int(n)] for o, n in zip(starts, lens)], C, 8)
+    yield A, B, table, point, want, lens
+    torch.cuda.synchronize()
+
+
+def test_hash_chunks_reads_a_large_pinned_table_during_the_call(big_tables):
+    A, B, table, point, want, lens = big_tables
+    point(A)
+    seg, n_leaves = hv.hv_leaf_layout(table[:, 0].copy(), table[:, 1].copy(), C)
+    out = torch.empty((n_leaves, 32), dtype=torch.uint8, device=DEV)
+    ws = hv.Workspace(DEV).get(hv.lib.hv_hash_workspace_bytes(N_BIG, n_leaves))
+    for _ in range(2):
+        busy()
+        st = hv.lib.hv_hash_chunks(table.ctypes.data, N_BIG, C, out.data_ptr(), ws.data_ptr(), ws.numel(),
+                                   hv._stream(DEV))
+        point(B)
+        torch.cuda.synchronize()
+        assert st == hv.HV_OK
+        assert np.array_equal(out.cpu().numpy(), want)
+        point(A)
+
+
+def test_a_refused_large_table_launches_nothing_and_the_workspace_stays_usable(big_tables):
+    A, B, table, point, want, lens = big_tables
+    point(A)
+    seg, n_leaves = hv.hv_leaf_layout(table[:, 0].copy(), table[:, 1].copy(), C)
+    out = torch.zeros((n_leaves, 32), dtype=torch.uint8, device=DEV)
+    ws = hv.Workspace(DEV).get(hv.lib.hv_hash_workspace_bytes(N_BIG, n_leaves))
+    bad = int(np.flatnonzero(lens)[-1])  # a message with bytes, late in the table
+    table[bad, 0] = 0
+    busy()
+    st = hv.lib.hv_hash_chunks(table.ctypes.data, N_BIG, C, out.data_ptr(), ws.data_ptr(), ws.numel(),
+                               hv._stream(DEV))
+    assert st == hv.HV_ERR_INVALID_ARG
+    assert f"message {bad} has NULL data".encode() in hv.lib.hv_last_error()
+    torch.cuda.synchronize()
+    assert not out.any()  # no leaf kernel ran
+    point(A)
+    st = hv.lib.hv_hash_chunks(table.ctypes.data, N_BIG, C, out.data_ptr(), ws.data_ptr(), ws.numel(),
+                               hv._stream(DEV))
+    torch.cuda.synchronize()
+    assert st == hv.HV_OK and np.array_equal(out.cpu().numpy(), want)

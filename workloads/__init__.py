@@ -143,6 +143,14 @@ class MessageSet:
     buffer: torch.Tensor | None = None    # one packed buffer holding every message, if any
     offsets: np.ndarray | None = None     # byte offsets of the messages in ``buffer``
 
+    def __post_init__(self):
+        # the message table is fixed once made: read-only arrays let a caller
+        # (the binding's Verifier) keep the descriptor table built from them
+        self.ptrs = np.asarray(self.ptrs, dtype=np.uint64)
+        self.lens = np.asarray(self.lens, dtype=np.uint64)
+        self.ptrs.flags.writeable = False
+        self.lens.flags.writeable = False
+
     @property
     def total_bytes(self) -> int:
         return int(self.lens.sum()) if len(self.lens) else 0
