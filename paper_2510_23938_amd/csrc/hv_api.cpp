@@ -103,11 +103,71 @@ hv_status refuse(const hv_msg* msgs, uint32_t m, uint64_t C, BadMsg why) {
 // Message tables at least this long are scanned by several host threads.
 constexpr uint32_t kParallelScanMin = 1u << 16;
 
+// Runs body(0 .. T-1), body(0) on the calling thread.  Returns false when the
+// host could not start every thread (the parts that ran are then incomplete).
+template <class F>
+bool run_parts(unsigned T, F&& body) {
+    std::vector<std::thread> pool;
+    bool started = true;
+    try {
+        pool.reserve(T - 1);
+        for (unsigned t = 1; t < T; ++t) pool.emplace_back(body, t);
+    } catch (...) {
+        started = false;
+    }
+    body(0u);
+    for (auto& th : pool) th.join();
+    return started;
+}
+
+enum class Parallel { kDone, kRefused, kUnavailable };
+
+// layout's pass split over T threads: counts per part, then (with
+// seg_offsets) the offsets of each part from its base.  kRefused: the lowest
+// refused message is reported through fail(); kUnavailable: threads could
+// not be started and nothing the caller keeps was written but seg_offsets
+// entries the single pass rewrites.
+Parallel parallel_layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_offsets, unsigned T,
+                         uint64_t* total_out, uint64_t* full_out) {
+    std::vector<uint64_t> leaves(T, 0), fulls(T, 0), base(T, 0);
+    std::vector<uint32_t> bad(T, 0);
+    std::vector<BadMsg> why(T, kNone);
+    auto part = [&](unsigned t) { return (uint32_t)((uint64_t)n_msgs * t / T); };
+    if (!run_parts(T, [&](unsigned t) {
+            why[t] = scan_messages(msgs, part(t), part(t + 1), C, 0, nullptr, &leaves[t], &fulls[t], &bad[t]);
+        }))
+        return Parallel::kUnavailable;
+    uint64_t total = 0, full = 0;
+    for (unsigned t = 0; t < T; ++t) {
+        if (why[t] != kNone) {
+            (void)refuse(msgs, bad[t], C, why[t]);
+            return Parallel::kRefused;
+        }
+        if (total + leaves[t] < total) {
+            (void)fail(HV_ERR_INVALID_ARG, "leaf count overflows");
+            return Parallel::kRefused;
+        }
+        base[t] = total;
+        total += leaves[t];
+        full += fulls[t];
+    }
+    if (seg_offsets && !run_parts(T, [&](unsigned t) {
+            uint64_t l, f;
+            uint32_t b;
+            (void)scan_messages(msgs, part(t), part(t + 1), C, base[t], seg_offsets, &l, &f, &b);
+        }))
+        return Parallel::kUnavailable;
+    *total_out = total;
+    *full_out = full;
+    return Parallel::kDone;
+}
+
 }  // namespace
 
 // Leaf counts of a message list; fills seg_offsets when given.  Large tables
-// are split over host threads; whatever the split, the error reported is the
-// one of the lowest refused message, as a single pass would report it.
+// are split over host threads (a single pass when threads cannot be started);
+// whatever the split, the error reported is the one of the lowest refused
+// message, as a single pass would report it.
 hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_offsets, uint64_t* n_leaves,
                  uint64_t* n_full) {
     if (n_msgs > 0 && msgs == nullptr) return fail(HV_ERR_INVALID_ARG, "msgs is NULL with n_msgs = %u", n_msgs);
@@ -120,46 +180,13 @@ hv_status layout(const hv_msg* msgs, uint32_t n_msgs, uint64_t C, uint64_t* seg_
         T = hw == 0 ? 1 : (hw < 16 ? hw : 16);
     }
     uint64_t total = 0, full = 0;
-    if (T <= 1) {
+    Parallel got = Parallel::kUnavailable;
+    if (T > 1) got = parallel_layout(msgs, n_msgs, C, seg_offsets, T, &total, &full);
+    if (got == Parallel::kRefused) return HV_ERR_INVALID_ARG;
+    if (got == Parallel::kUnavailable) {
         uint32_t bad = 0;
         const BadMsg why = scan_messages(msgs, 0, n_msgs, C, 0, seg_offsets, &total, &full, &bad);
         if (why != kNone) return refuse(msgs, bad, C, why);
-    } else {
-        // pass 1: counts per part (no offsets); pass 2: offsets from each part's base
-        std::vector<uint64_t> leaves(T, 0), fulls(T, 0);
-        std::vector<uint32_t> bad(T, 0);
-        std::vector<BadMsg> why(T, kNone);
-        auto part = [&](unsigned t) { return (uint32_t)((uint64_t)n_msgs * t / T); };
-        {
-            std::vector<std::thread> pool;
-            for (unsigned t = 1; t < T; ++t)
-                pool.emplace_back([&, t] {
-                    why[t] = scan_messages(msgs, part(t), part(t + 1), C, 0, nullptr, &leaves[t], &fulls[t], &bad[t]);
-                });
-            why[0] = scan_messages(msgs, part(0), part(1), C, 0, nullptr, &leaves[0], &fulls[0], &bad[0]);
-            for (auto& th : pool) th.join();
-        }
-        std::vector<uint64_t> base(T, 0);
-        for (unsigned t = 0; t < T; ++t) {
-            if (why[t] != kNone) return refuse(msgs, bad[t], C, why[t]);
-            if (total + leaves[t] < total) return fail(HV_ERR_INVALID_ARG, "leaf count overflows");
-            base[t] = total;
-            total += leaves[t];
-            full += fulls[t];
-        }
-        if (seg_offsets) {
-            std::vector<std::thread> pool;
-            uint64_t unused_leaves, unused_full;
-            uint32_t unused_bad;
-            for (unsigned t = 1; t < T; ++t)
-                pool.emplace_back([&, t] {
-                    uint64_t l, f;
-                    uint32_t b;
-                    (void)scan_messages(msgs, part(t), part(t + 1), C, base[t], seg_offsets, &l, &f, &b);
-                });
-            (void)scan_messages(msgs, part(0), part(1), C, 0, seg_offsets, &unused_leaves, &unused_full, &unused_bad);
-            for (auto& th : pool) th.join();
-        }
     }
     *n_leaves = total;
     if (n_full) *n_full = full;
@@ -284,15 +311,41 @@ namespace {
 // A descriptor upload started before the host validates the table, so that
 // the DMA runs under the validation.  The host array is consumed once wait()
 // returns; every path out of a call that started one goes through wait().
-thread_local hipEvent_t g_upload_event = nullptr;  // one per thread, kept for the thread's life
-constexpr uint32_t kEarlyUploadMin = 4096;           // smaller tables upload in a few microseconds
+constexpr uint32_t kEarlyUploadMin = 4096;  // smaller tables upload in a few microseconds
+constexpr int kEventDevices = 64;
+thread_local hipEvent_t g_upload_event[kEventDevices] = {};  // per thread and device, kept for the thread's life
+
+// This thread's upload event for the device that owns `stream` (an event
+// records only on streams of the device it was made on).
+hipError_t upload_event(hipStream_t stream, hipEvent_t* ev) {
+    int dev = -1;
+    hipError_t e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kEventDevices) return hipErrorInvalidDevice;
+    if (g_upload_event[dev] == nullptr) {
+        int cur = -1;
+        if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        hipEvent_t made = nullptr;
+        e = hipEventCreateWithFlags(&made, hipEventDisableTiming);
+        if (cur != dev) {
+            const hipError_t back = hipSetDevice(cur);
+            if (e == hipSuccess) e = back;
+        }
+        if (e != hipSuccess) return e;
+        g_upload_event[dev] = made;
+    }
+    *ev = g_upload_event[dev];
+    return hipSuccess;
+}
 
 struct Upload {
+    hipEvent_t ev = nullptr;
     bool pending = false;
     hv_status wait(hv_status st) {
         if (!pending) return st;
         pending = false;
-        const hipError_t e = hipEventSynchronize(g_upload_event);
+        const hipError_t e = hipEventSynchronize(ev);
         return st == HV_OK && e != hipSuccess ? hip_fail(e, "descriptor upload") : st;
     }
 };
@@ -311,12 +364,11 @@ hv_status schedule(const hv_msg* msgs, uint32_t n_msgs, uint64_t chunk_bytes, bo
     if (early_upload && n_msgs >= kEarlyUploadMin && msgs != nullptr && chunk_bytes % 64 == 0 &&
         workspace != nullptr && (uintptr_t)workspace % kAlign == 0 &&
         workspace_bytes >= round_up(sizeof(hv_msg) * (size_t)n_msgs)) {
-        hipError_t e = hipSuccess;
-        if (g_upload_event == nullptr) e = hipEventCreateWithFlags(&g_upload_event, hipEventDisableTiming);
+        hipError_t e = upload_event(stream, &up->ev);
         if (e == hipSuccess) e = hipMemcpyAsync(workspace, msgs, sizeof(hv_msg) * n_msgs, hipMemcpyHostToDevice, stream);
         if (e == hipSuccess) {
             up->pending = true;
-            e = hipEventRecord(g_upload_event, stream);
+            e = hipEventRecord(up->ev, stream);
             if (e != hipSuccess) {
                 // no event to wait on: wait for the stream itself before the host array is released
                 up->pending = false;

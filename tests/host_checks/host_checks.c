@@ -92,6 +92,40 @@ static void layouts_and_sizes(void) {
     }
 }
 
+/* Tables of 2^16 messages or more are validated on several host threads:
+ * the same offsets as the per-message rule, and the lowest refused message. */
+static void large_layouts(void) {
+    enum { N = 150000 };
+    static hv_msg m[N];
+    static uint64_t seg[N + 1];
+    for (int t = 0; t < 6; ++t) {
+        const uint64_t C = t % 3 == 0 ? 0 : 4096ull << (t % 3);
+        random_set(m, N, C, 1u << 18);
+        uint64_t n_leaves = 0, want = 0;
+        CHECK(hv_leaf_layout(m, N, C, seg, &n_leaves) == HV_OK);
+        CHECK(seg[0] == 0);
+        for (uint32_t i = 0; i < N; ++i) {
+            want += m[i].nbytes == 0 && C ? 0 : leaves_of(m[i].nbytes, C);
+            CHECK(seg[i + 1] == want);
+        }
+        CHECK(n_leaves == want);
+        CHECK(hv_leaf_layout(m, N, C, NULL, &n_leaves) == HV_OK && n_leaves == want);
+        /* two refused messages: the lower one is reported */
+        const uint32_t a = (uint32_t)(next() % N), b = (uint32_t)(next() % N);
+        const hv_msg ka = m[a], kb = m[b];
+        m[a].data = NULL;
+        m[a].nbytes = 1;
+        m[b].data = NULL;
+        m[b].nbytes = 1;
+        REJECTED(hv_leaf_layout(m, N, C, seg, &n_leaves), HV_ERR_INVALID_ARG);
+        char want_msg[64];
+        snprintf(want_msg, sizeof want_msg, "message %u has NULL data", a < b ? a : b);
+        CHECK(strstr(hv_last_error(), want_msg) != NULL);
+        m[a] = ka;
+        m[b] = kb;
+    }
+}
+
 static void stream_plans(void) {
     static hv_msg m[64];
     for (int t = 0; t < 500; ++t) {
@@ -260,6 +294,7 @@ static void rejections(void) {
 
 int main(void) {
     layouts_and_sizes();
+    large_layouts();
     stream_plans();
     tree_sizes();
     rejections();

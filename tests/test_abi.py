@@ -501,3 +501,39 @@ def test_descriptor_table_cache_only_for_read_only_arrays():
     other = lens.copy()
     other.flags.writeable = False
     assert cache.lookup(ptrs, other, 0)[0] is not arr2  # an equal but different array object: rebuilt
+
+
+_NO_THREADS = r"""
+import sys, resource, ctypes, threading, numpy as np
+sys.path.insert(0, sys.argv[1])
+from paper_2510_23938_amd import hv
+n = 300_000
+lens = np.random.default_rng(3).integers(0, 70000, n).astype(np.uint64)
+ptrs = np.uint64(1 << 40) + np.arange(n, dtype=np.uint64) * np.uint64(1 << 17)
+arr = hv._msg_array(ptrs, lens)
+seg = np.zeros(n + 1, dtype=np.uint64)
+bad = arr.copy()
+bad[200_000, 0] = 0
+want = np.concatenate([[0], np.cumsum((lens + np.uint64(4095)) // np.uint64(4096))]).astype(np.uint64)
+with open("/proc/self/statm") as f:
+    vm = int(f.read().split()[0]) * resource.getpagesize()
+resource.setrlimit(resource.RLIMIT_AS, (vm + (6 << 20), resource.RLIM_INFINITY))  # no room for a thread stack
+try:
+    threading.Thread(target=lambda: None).start()
+    sys.exit(3)  # threads still start: the check would prove nothing
+except RuntimeError:
+    pass
+nl = ctypes.c_uint64(0)
+assert hv.lib.hv_leaf_layout(arr.ctypes.data, n, 4096, seg.ctypes.data, ctypes.byref(nl)) == hv.HV_OK
+assert nl.value == int(want[-1]) and np.array_equal(seg, want)
+assert hv.lib.hv_leaf_layout(bad.ctypes.data, n, 4096, None, ctypes.byref(nl)) == hv.HV_ERR_INVALID_ARG
+assert b"message 200000 has NULL data" in hv.lib.hv_last_error()
+"""
+
+
+def test_large_tables_fall_back_to_one_pass_when_threads_cannot_start():
+    import subprocess
+    import sys
+
+    r = subprocess.run([sys.executable, "-c", _NO_THREADS, ROOT], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, (r.returncode, r.stderr[-2000:])
