@@ -242,10 +242,10 @@ uint64_t merkle_tiles_bound(uint64_t n_nodes, uint32_t n_seg) {
 hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches) {
     const size_t row = (size_t)n_seg + 1;
     table->assign(seg_offsets, seg_offsets + row);
-    const bool grouped = merkle_grouped(seg_offsets[n_seg]);
     int k = 0;
     for (;;) {
-        const uint64_t w = grouped && k == 0 ? (uint64_t)hv::kGroupNodes : (uint64_t)hv::kTileNodes;
+        const uint64_t entries = (*table)[(size_t)k * row + n_seg];
+        const uint64_t w = merkle_grouped(entries) ? (uint64_t)hv::kGroupNodes : (uint64_t)hv::kTileNodes;
         std::vector<uint64_t> next(row);
         next[0] = 0;
         bool more = false;
@@ -270,15 +270,15 @@ hv_status queue_merkle(hv_alg alg, const uint8_t* in, uint8_t* out, const uint64
                        hipStream_t stream) {
     const size_t row = (size_t)n_seg + 1;
     const int a = alg == HV_SHA384 ? hv::kAlgSha384 : hv::kAlgSha256;
-    const bool grouped = merkle_grouped(n_nodes);
     for (int k = 1; k <= launches; ++k) {
         uint8_t* dst = k == launches ? out : (k % 2 ? ping : pong);
         const uint64_t* in_off = table + (size_t)(k - 1) * row;
         const uint64_t* out_off = table + (size_t)k * row;
-        const hipError_t e = grouped && k == 1
-                                 ? hv::launch_merkle_groups(a, in, dst, in_off, out_off, n_seg, outputs[0], 1, stream)
-                                 : hv::launch_merkle_tiles(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1,
-                                                           stream);
+        const uint64_t entries = k == 1 ? n_nodes : outputs[k - 2];  // the plan's rule, from the same counts
+        const hipError_t e =
+            merkle_grouped(entries)
+                ? hv::launch_merkle_groups(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1, stream)
+                : hv::launch_merkle_tiles(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1, stream);
         if (e != hipSuccess) return hip_fail(e, "merkle kernel");
         in = dst;
     }

@@ -69,11 +69,11 @@ hv_status hash_chunks_into(hv_alg alg, const hv_msg* msgs, uint32_t n_msgs, uint
 hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t chunk_bytes, uint64_t n_full,
                          uint64_t n_leaves, const HashLayout& L, hipStream_t stream);
 
-// Segmented Merkle reductions chain launches.  A reduction of at least
-// kGroupMinNodes entries starts with a group launch (3 levels in registers,
-// one lane per group of 8 entries: every lane busy on the widest levels);
-// every other launch takes 9 levels (512-node tiles).  A 64-bit node count
-// needs at most 1 + ceil(61 / 9) = 8 launches.
+// Segmented Merkle reductions chain launches.  A launch whose input has at
+// least kGroupMinNodes entries is a group launch (3 levels in registers, one
+// lane per group of 8 entries: every lane busy on the widest levels); every
+// other launch takes 9 levels (512-node tiles).  Up to 2^31 entries (the
+// per-call limit) that is at most 5 group launches and 2 tile launches.
 constexpr int kMaxMerkleLaunches = 8;
 constexpr uint64_t kGroupMinNodes = (uint64_t)1 << 18;
 inline bool merkle_grouped(uint64_t n_nodes) { return n_nodes >= kGroupMinNodes; }
@@ -82,8 +82,8 @@ inline bool merkle_grouped(uint64_t n_nodes) { return n_nodes >= kGroupMinNodes;
 // `table` gets rows of n_seg + 1 offsets -- row 0 the segment offsets, row k
 // the first output node of each segment after launch k (a segment with c
 // nodes gets max(1, ceil(c / w)) outputs, w = 8 for a group launch, else
-// 512) -- and `launches` the launch count.  The first launch is a group
-// launch exactly when merkle_grouped(seg_offsets[n_seg]).
+// 512) -- and `launches` the launch count.  Launch k is a group launch
+// exactly when merkle_grouped(entries of row k - 1).
 hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches);
 
 // Nodes any launch of a reduction of n_nodes nodes in n_seg segments writes, at most.

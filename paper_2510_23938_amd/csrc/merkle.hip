@@ -20,12 +20,12 @@
 // (64 nodes down to one) stay in wave 0 and exchange children by cross-lane
 // shuffles.
 //
-// A large reduction (at least 2^18 entries) first runs a group launch (below):
-// one lane per aligned group of 8 entries, three levels in registers, so that
-// the widest levels keep every lane busy; the tile launches then start from
-// the group nodes.  The tile kernel alone leaves lanes idle on its top levels
-// and costs more for the same nodes: on the 70B-shaped set (2.15 M leaves in
-// 723 segments) groups first cut the per-tensor reduction by about a quarter.
+// Levels of at least 2^18 entries run as group launches instead (below): one
+// lane per aligned group of 8 entries, three levels in registers, so that the
+// widest levels keep every lane busy; the tile launches then start from the
+// group nodes.  The tile kernel alone leaves lanes idle on its top levels and
+// costs more for the same nodes: on the 70B-shaped set (2.15 M leaves in 723
+// segments, two group launches) the per-tensor reduction takes about 30% less.
 //
 // The kernels are written once over a node-hash policy: SHA-256 (32-byte nodes;
 // an interior node is two blocks) or SHA-384 (48-byte nodes; leaf and
@@ -131,7 +131,7 @@ __global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t*
     }
 }
 
-// The first launch of a large reduction (the host plans it for 2^18 entries or more):
+// A launch over a level of 2^18 entries or more (the host plans which):
 // lane g reduces group g of its segment -- entries [8t, min(8t + 8, c)) for
 // the segment's t-th group, c its entry count -- to one node in registers,
 // forming the leaf hashes first in leaf mode.  Groups start at multiples of

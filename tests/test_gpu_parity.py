@@ -169,7 +169,29 @@ def test_merkle_group_launch_every_segment_size(alg, big_first):
     assert [bytes(r) for r in part_roots.cpu().numpy()] == want[lo:lo + len(small)]
 
 
-@pytest.mark.parametrize("n", [(1 << 18) - 1, 1 << 18, (1 << 18) + 1, (1 << 18) + 7, 3 * (1 << 18) + 5])
+@pytest.mark.parametrize("alg", ["sha256", "sha384"])
+def test_merkle_two_group_launches_every_segment_size(alg):
+    # a level of 2^18 nodes or more also runs as a group launch: here the
+    # level-3 nodes (about 285,000) too, so the second group launch meets every
+    # short last group of the segments of sizes 0..600 reduced once already
+    D = 32 if alg == "sha256" else 48
+    sizes = list(range(601)) + [2_100_007]
+    n = sum(sizes)
+    groups = sum(max(1, -(-c // 8)) for c in sizes)
+    assert groups >= 1 << 18
+    entries = W.random_bytes(n * D, 280 + D, DEV).view(n, D)
+    seg = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    roots = hv.hv_merkle_reduce(entries, seg, alg=alg)
+    torch.cuda.synchronize()
+    host = entries.cpu().numpy()
+    want = [oracle.mth(host[int(seg[k]):int(seg[k + 1])], alg) for k in range(len(sizes))]
+    got = [bytes(r) for r in roots.cpu().numpy()]
+    bad = [sizes[k] for k in range(len(sizes)) if got[k] != want[k]]
+    assert not bad, f"{alg}: roots differ for segment sizes {bad[:10]}"
+
+
+@pytest.mark.parametrize("n", [(1 << 18) - 1, 1 << 18, (1 << 18) + 1, (1 << 18) + 7, 3 * (1 << 18) + 5,
+                               (1 << 21) - 8, (1 << 21) - 7, (1 << 21) + 1])
 def test_merkle_single_tree_around_the_group_threshold(n):
     entries = W.random_bytes(n * 32, 270 + n % 97, DEV).view(n, 32)
     root = hv.hv_merkle_reduce(entries, np.array([0, n], dtype=np.uint64))
