@@ -1,5 +1,6 @@
 /*
- * hv_inspect.h -- inspection entry point for tests of the chunk scheduler.
+ * hv_inspect.h -- inspection entry points for tests: the chunk scheduler's
+ * leaf table, the leaf-kernel choice and the Merkle launch plan.
  *
  * hv_leaf_schedule runs the same device-side scheduling hv_hash_chunks runs
  * (Algorithm 1's chunking: ceil(|M| / C) chunks per message, the last one
@@ -45,6 +46,24 @@ hv_status hv_set_leaf_kernel(int choice);
  * scans take the one-wave kernel under the automatic choice.
  * Errors: HV_ERR_INVALID_ARG for a NULL kernel. */
 hv_status hv_leaf_kernel_for(uint64_t n_leaves, int* kernel);
+
+/* The launches hv_merkle_reduce_alg makes for these segments on the current
+ * device (RFC 6962 section 2.1's tree, built level by level; Algorithm 1's
+ * "construct Merkle tree from leaf_hashes using GPU"), for tests and
+ * measurements: *launches (at most 8), and per launch k < *launches
+ * kind[k] = 1 for a group launch (8 entries of a segment reduced by three
+ * levels in registers), 2 for a tile launch (512 entries, nine levels) or 3
+ * for a wide tile launch (1024 entries, ten levels: the last launch over one
+ * segment of 513..1024 entries),
+ * units[k] = the groups or tiles it reduces, and one_lane[k] = the groups a
+ * group launch gives one lane each; its remaining units[k] - one_lane[k]
+ * groups, the launch's last ones, take four lanes each (0 for a tile
+ * launch).  kind, units and one_lane: host arrays of at least 8 entries.
+ * Host only; no kernel runs.  Errors: HV_ERR_INVALID_ARG as
+ * hv_merkle_reduce_alg's checks of alg and seg_offsets, or for a NULL output;
+ * HV_ERR_HIP if the device cannot be queried. */
+hv_status hv_merkle_launches(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, int* launches, int* kind,
+                             uint64_t* units, uint64_t* one_lane);
 
 #ifdef __cplusplus
 }

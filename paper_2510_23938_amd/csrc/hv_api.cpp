@@ -9,6 +9,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <thread>
 #include <vector>
 
@@ -239,13 +240,25 @@ uint64_t merkle_tiles_bound(uint64_t n_nodes, uint32_t n_seg) {
     return n_nodes / w + (uint64_t)n_seg + 1;
 }
 
+hv_status check_segments(const uint64_t* seg_offsets, uint32_t n_seg) {
+    if (seg_offsets[0] != 0) return fail(HV_ERR_INVALID_ARG, "seg_offsets[0] = %llu, not 0",
+                                         (unsigned long long)seg_offsets[0]);
+    for (uint32_t s = 0; s < n_seg; ++s)
+        if (seg_offsets[s + 1] < seg_offsets[s])
+            return fail(HV_ERR_INVALID_ARG, "seg_offsets decreases at segment %u", s);
+    if (seg_offsets[n_seg] > kMaxLeaves)
+        return fail(HV_ERR_INVALID_ARG, "%llu entries exceed the per-call limit",
+                    (unsigned long long)seg_offsets[n_seg]);
+    return HV_OK;
+}
+
 hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches) {
     const size_t row = (size_t)n_seg + 1;
     table->assign(seg_offsets, seg_offsets + row);
     int k = 0;
     for (;;) {
         const uint64_t entries = (*table)[(size_t)k * row + n_seg];
-        const uint64_t w = merkle_grouped(entries) ? (uint64_t)hv::kGroupNodes : (uint64_t)hv::kTileNodes;
+        const uint64_t w = merkle_width(entries, n_seg);
         std::vector<uint64_t> next(row);
         next[0] = 0;
         bool more = false;
@@ -265,20 +278,75 @@ hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<u
     return HV_OK;
 }
 
+namespace {
+
+constexpr int kCuDevices = 64;
+std::atomic<uint32_t> g_cus[kCuDevices];  // compute units per device, 0 until asked
+
+// Compute units of device `dev`, asked once per device.
+hipError_t device_cus(int dev, uint32_t* cus) {
+    if (dev < 0 || dev >= kCuDevices) return hipErrorInvalidDevice;
+    uint32_t n = g_cus[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        int v = 0;
+        const hipError_t e = hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess) return e;
+        n = v > 0 ? (uint32_t)v : 0u;
+        g_cus[dev].store(n, std::memory_order_relaxed);
+    }
+    *cus = n;
+    return hipSuccess;
+}
+
+hipError_t stream_cus(hipStream_t stream, uint32_t* cus) {
+    int dev = -1;
+    const hipError_t e = hipStreamGetDevice(stream, &dev);
+    return e != hipSuccess ? e : device_cus(dev, cus);
+}
+
+}  // namespace
+
+hv_status merkle_launch_kinds(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, int dev, int* launches,
+                              int* kind, uint64_t* units, uint64_t* one_lane) {
+    std::vector<uint64_t> table;
+    hv_status st = merkle_plan(seg_offsets, n_seg, &table, launches);
+    if (st != HV_OK) return st;
+    const size_t row = (size_t)n_seg + 1;
+    uint32_t cus = 0;
+    for (int k = 1; k <= *launches; ++k) {
+        const uint64_t entries = table[(size_t)(k - 1) * row + n_seg], out = table[(size_t)k * row + n_seg];
+        const bool grouped = merkle_grouped(entries);
+        if (grouped && cus == 0) {
+            const hipError_t e = device_cus(dev, &cus);
+            if (e != hipSuccess) return hip_fail(e, "device query");
+        }
+        kind[k - 1] = grouped ? 1 : merkle_wide(entries, n_seg) ? 3 : 2;
+        units[k - 1] = out;
+        one_lane[k - 1] = grouped ? merkle_group_main(out, k == 1, alg == HV_SHA384, cus) : 0;
+    }
+    return HV_OK;
+}
+
 hv_status queue_merkle(hv_alg alg, const uint8_t* in, uint8_t* out, const uint64_t* table, uint32_t n_seg,
                        uint64_t n_nodes, int launches, const uint64_t* outputs, uint8_t* ping, uint8_t* pong,
                        hipStream_t stream) {
     const size_t row = (size_t)n_seg + 1;
     const int a = alg == HV_SHA384 ? hv::kAlgSha384 : hv::kAlgSha256;
+    uint32_t cus = 0;
     for (int k = 1; k <= launches; ++k) {
         uint8_t* dst = k == launches ? out : (k % 2 ? ping : pong);
         const uint64_t* in_off = table + (size_t)(k - 1) * row;
         const uint64_t* out_off = table + (size_t)k * row;
         const uint64_t entries = k == 1 ? n_nodes : outputs[k - 2];  // the plan's rule, from the same counts
-        const hipError_t e =
-            merkle_grouped(entries)
-                ? hv::launch_merkle_groups(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1, stream)
-                : hv::launch_merkle_tiles(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1, stream);
+        hipError_t e;
+        if (merkle_grouped(entries)) {
+            if (cus == 0 && (e = stream_cus(stream, &cus)) != hipSuccess) return hip_fail(e, "device query");
+            const uint64_t n_main = merkle_group_main(outputs[k - 1], k == 1, alg == HV_SHA384, cus);
+            e = hv::launch_merkle_groups(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], n_main, k == 1, stream);
+        } else {
+            e = hv::launch_merkle_tiles(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1,
+                                        merkle_wide(entries, n_seg), stream);
+        }
         if (e != hipSuccess) return hip_fail(e, "merkle kernel");
         in = dst;
     }
@@ -499,14 +567,9 @@ hv_status hv_merkle_reduce_alg(hv_alg alg, const uint8_t* nodes, const uint64_t*
     if (n_seg == 0) return fail(HV_ERR_INVALID_ARG, "n_seg is 0");
     if (seg_offsets == nullptr) return fail(HV_ERR_INVALID_ARG, "seg_offsets is NULL");
     if (roots == nullptr) return fail(HV_ERR_INVALID_ARG, "roots is NULL");
-    if (seg_offsets[0] != 0) return fail(HV_ERR_INVALID_ARG, "seg_offsets[0] = %llu, not 0",
-                                         (unsigned long long)seg_offsets[0]);
-    for (uint32_t s = 0; s < n_seg; ++s)
-        if (seg_offsets[s + 1] < seg_offsets[s])
-            return fail(HV_ERR_INVALID_ARG, "seg_offsets decreases at segment %u", s);
+    hv_status st = check_segments(seg_offsets, n_seg);
+    if (st != HV_OK) return st;
     const uint64_t n_nodes = seg_offsets[n_seg];
-    if (n_nodes > kMaxLeaves) return fail(HV_ERR_INVALID_ARG, "%llu entries exceed the per-call limit",
-                                          (unsigned long long)n_nodes);
     if (n_nodes > 0 && nodes == nullptr) return fail(HV_ERR_INVALID_ARG, "nodes is NULL");
     if ((uintptr_t)nodes % 16 != 0 || (uintptr_t)roots % 16 != 0)
         return fail(HV_ERR_INVALID_ARG, "nodes and roots must be 16-byte aligned");
@@ -520,8 +583,7 @@ hv_status hv_merkle_reduce_alg(hv_alg alg, const uint8_t* nodes, const uint64_t*
     const size_t row = (size_t)n_seg + 1;
     std::vector<uint64_t> table;
     int launches = 0;
-    const hv_status st = merkle_plan(seg_offsets, n_seg, &table, &launches);
-    if (st != HV_OK) return st;
+    if ((st = merkle_plan(seg_offsets, n_seg, &table, &launches)) != HV_OK) return st;
 
     const MerkleLayout L = merkle_layout(workspace, n_nodes, n_seg, D);
     const hipError_t e = hipMemcpyWithStream(L.table, table.data(), table.size() * sizeof(uint64_t),
@@ -619,6 +681,20 @@ hv_status hv_leaf_kernel_for(uint64_t n_leaves, int* kernel) {
     if (kernel == nullptr) return fail(HV_ERR_INVALID_ARG, "kernel is NULL");
     *kernel = hv::leaf_kernel_for(n_leaves, false);
     return HV_OK;
+}
+
+hv_status hv_merkle_launches(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, int* launches, int* kind,
+                             uint64_t* units, uint64_t* one_lane) {
+    if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
+    if (n_seg == 0) return fail(HV_ERR_INVALID_ARG, "n_seg is 0");
+    if (seg_offsets == nullptr || launches == nullptr || kind == nullptr || units == nullptr || one_lane == nullptr)
+        return fail(HV_ERR_INVALID_ARG, "seg_offsets, launches, kind, units and one_lane must be non-NULL");
+    hv_status st = check_segments(seg_offsets, n_seg);
+    if (st != HV_OK) return st;
+    int dev = -1;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "device query");
+    return merkle_launch_kinds(alg, seg_offsets, n_seg, dev, launches, kind, units, one_lane);
 }
 
 hv_status hv_set_kernel_timing(int enable) {

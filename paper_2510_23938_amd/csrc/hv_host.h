@@ -77,14 +77,56 @@ hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t 
 constexpr int kMaxMerkleLaunches = 8;
 constexpr uint64_t kGroupMinNodes = (uint64_t)1 << 18;
 inline bool merkle_grouped(uint64_t n_nodes) { return n_nodes >= kGroupMinNodes; }
+// A tile launch over one segment of 513..1024 entries takes one 1024-node
+// tile and finishes the tree, where 512-node tiles would need a second
+// launch for one level.
+inline bool merkle_wide(uint64_t n_nodes, uint32_t n_seg) {
+    return n_seg == 1 && n_nodes > (uint64_t)hv::kTileNodes && n_nodes <= (uint64_t)hv::kWideTileNodes;
+}
+// Entries one output node of a launch over n_nodes entries in n_seg segments covers.
+inline uint64_t merkle_width(uint64_t n_nodes, uint32_t n_seg) {
+    return merkle_grouped(n_nodes) ? (uint64_t)hv::kGroupNodes
+           : merkle_wide(n_nodes, n_seg) ? (uint64_t)hv::kWideTileNodes
+                                         : (uint64_t)hv::kTileNodes;
+}
 
 // Host plan of a segmented Merkle reduction over validated segment offsets:
 // `table` gets rows of n_seg + 1 offsets -- row 0 the segment offsets, row k
 // the first output node of each segment after launch k (a segment with c
-// nodes gets max(1, ceil(c / w)) outputs, w = 8 for a group launch, else
-// 512) -- and `launches` the launch count.  Launch k is a group launch
-// exactly when merkle_grouped(entries of row k - 1).
+// nodes gets max(1, ceil(c / w)) outputs, w = merkle_width(entries of row
+// k - 1)) -- and `launches` the launch count.  Launch k is a group launch
+// exactly when merkle_grouped(entries of row k - 1), and a wide tile launch
+// when merkle_wide(...).
 hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches);
+
+// Segment offsets: start at 0, never decrease, at most the per-call entry limit.
+hv_status check_segments(const uint64_t* seg_offsets, uint32_t n_seg);
+
+// The launches a reduction of these (checked) segments makes on device `dev`
+// (hv_merkle_launches in hv_inspect.h).
+hv_status merkle_launch_kinds(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, int dev, int* launches,
+                              int* kind, uint64_t* units, uint64_t* one_lane);
+
+// Groups a group launch of n_groups groups gives one lane each (the rest, its
+// last groups, get four lanes each), for a device of `cus` compute units
+// (4 SIMDs each).  A wave of one-lane groups takes D block times (8 entries:
+// the leaf hashes in leaf mode, then 7 nodes), a wave of four-lane groups d
+// (2 entries, then 3 nodes along the chain) for a quarter of the groups.
+// With R = 256 * cus groups per wave on every SIMD, all one-lane costs
+// ceil(G / R) * D on the busiest SIMD; the split keeps floor(G / R) whole
+// rounds and spreads the rest as four-lane waves, k * D + ceil(4r / R) * d.
+// The split is taken when it costs less: it shortens the launch's last round,
+// where one wave per SIMD would otherwise run alone.
+inline uint64_t merkle_group_main(uint64_t n_groups, bool leaf_mode, bool sha384, uint32_t cus) {
+    if (cus == 0) return n_groups;
+    const uint64_t leaf = leaf_mode ? 1 : 0, node = sha384 ? 1 : 2;  // 64- or 128-byte blocks per hash
+    const uint64_t D = 8 * leaf + 7 * node, d = 2 * leaf + 3 * node;
+    const uint64_t R = 256 * (uint64_t)cus;
+    const uint64_t k = n_groups / R, r = n_groups % R;
+    if (k == 0 || r == 0) return n_groups;
+    const uint64_t all = (k + 1) * D, split = k * D + (4 * r + R - 1) / R * d;
+    return split < all ? k * R : n_groups;
+}
 
 // Nodes any launch of a reduction of n_nodes nodes in n_seg segments writes, at most.
 uint64_t merkle_tiles_bound(uint64_t n_nodes, uint32_t n_seg);

@@ -104,20 +104,25 @@ hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t
 
 // Merkle tiles (merkle.hip).  One launch reduces every segment by up to
 // kTileLevels levels: tile t covers up to 2^kTileLevels consecutive nodes of
-// one segment and writes one node.
+// one segment and writes one node.  A wide launch takes tiles of
+// kWideTileNodes (one more level).
 constexpr int kTileLevels = 9;
 constexpr int kTileNodes = 1 << kTileLevels;
+constexpr int kWideTileNodes = 2 * kTileNodes;
 hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
-                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode,
+                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode, int wide,
                                hipStream_t s);
-// Merkle groups (merkle.hip), the first launch of a large reduction: one lane
-// reduces group g -- up to 2^kGroupLevels consecutive nodes of one segment,
-// starting at a multiple of that -- to one node, in registers.
+// Merkle groups (merkle.hip), the launches over the widest levels: group g
+// -- up to 2^kGroupLevels consecutive nodes of one segment, starting at a
+// multiple of that -- is reduced to one node in registers, by one lane for
+// g < n_main and by four lanes (two entries each, then two shuffle levels)
+// for the launch's last groups, g >= n_main.
 constexpr int kGroupLevels = 3;
 constexpr int kGroupNodes = 1 << kGroupLevels;
+constexpr int kGroupQuad = 4;  // lanes per group beyond n_main
 hipError_t launch_merkle_groups(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
-                                const uint64_t* grp_off, uint32_t n_seg, uint64_t n_groups, int leaf_mode,
-                                hipStream_t s);
+                                const uint64_t* grp_off, uint32_t n_seg, uint64_t n_groups, uint64_t n_main,
+                                int leaf_mode, hipStream_t s);
 
 // Persistent tree for incremental updates (tree.hip).
 hipError_t launch_tree_leaf_level(int alg, const uint8_t* digests, uint64_t n, uint8_t* level0, hipStream_t s);

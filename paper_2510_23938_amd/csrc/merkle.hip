@@ -48,21 +48,29 @@ __device__ __forceinline__ uint32_t find_segment(const uint64_t* __restrict__ ti
     return lo;
 }
 
-template <class T>
-__global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t* __restrict__ in, uint8_t* __restrict__ out,
-                                                               const uint64_t* __restrict__ in_off,
-                                                               const uint64_t* __restrict__ tile_off, uint32_t n_seg,
-                                                               uint64_t n_tiles, int leaf_mode) {
+// Tiles of 2 * Threads nodes: 512 (Threads = 256) in general, 1024 (512
+// threads) for a last launch over one segment of 513..1024 entries, which
+// then needs no second launch for its tenth level.  Four 512-node tiles per CU
+// where LDS allows (SHA-384 nodes); with SHA-256 the node-tail table (33 KB)
+// beside the 8 KB of level exchange leaves room for three.
+template <class T, int Threads>
+__global__ void __launch_bounds__(Threads, Threads > kThreads ? 1 : (T::kTableWords > 4 ? 3 : 4))
+    merkle_tile_kernel(const uint8_t* __restrict__ in, uint8_t* __restrict__ out, const uint64_t* __restrict__ in_off,
+                       const uint64_t* __restrict__ tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode) {
     constexpr int NW = T::kWords;
     constexpr int NB = T::kBytes;
-    __shared__ uint32_t lds[NW][kThreads];  // word-major: node i's word w at lds[w][i]
+    constexpr uint32_t Nodes = 2 * Threads;
+    __shared__ uint32_t lds[NW][Threads];  // word-major: node i's word w at lds[w][i]
+    __shared__ __align__(16) uint32_t tab[T::kTableWords];
     const uint32_t i = threadIdx.x;
+    T::stage_table(tab);
+    __syncthreads();
     for (uint64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
         const uint32_t s = find_segment(tile_off, n_seg, tile);
         const uint64_t t = tile - tile_off[s];
         const uint64_t c = in_off[s + 1] - in_off[s];
-        const uint64_t first = t * kTileNodes;
-        const uint32_t cnt = c > first ? (uint32_t)(c - first < (uint64_t)kTileNodes ? c - first : kTileNodes) : 0u;
+        const uint64_t first = t * Nodes;
+        const uint32_t cnt = c > first ? (uint32_t)(c - first < (uint64_t)Nodes ? c - first : Nodes) : 0u;
         const uint8_t* base = in + NB * (in_off[s] + first);
 
         uint32_t P[NW] = {};  // lanes without a node feed zeros to the shuffles
@@ -80,7 +88,7 @@ __global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t*
             if (hasB) {
                 T::load(base + 2 * NB * i + NB, B);
                 if (leaf_mode) { uint32_t X[NW]; T::leaf_hash(B, X); for (int w = 0; w < NW; ++w) B[w] = X[w]; }
-                T::node_hash(A, B, P);
+                T::node_hash(A, B, P, tab);
             } else if (hasA) {
                 for (int w = 0; w < NW; ++w) P[w] = A[w];  // unpaired last node moves up
             }
@@ -98,7 +106,7 @@ __global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t*
                 if (2 * i + 1 < n) {
                     uint32_t R[NW];
                     for (int w = 0; w < NW; ++w) R[w] = lds[w][2 * i + 1];
-                    T::node_hash(L, R, P);
+                    T::node_hash(L, R, P, tab);
                 } else {
                     for (int w = 0; w < NW; ++w) P[w] = L[w];
                 }
@@ -109,6 +117,10 @@ __global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t*
         // The rest of the tile lies in wave 0's lanes: children come from
         // lanes 2k and 2k+1 by cross-lane shuffles, with no barrier.  Every
         // lane of the wave takes part in the shuffles; only lanes k < m hash.
+        // A wide tile is a reduction's last launch, alone on the chip, where
+        // one wave's latency is the time: there every lane hashes (a wave
+        // with few active lanes runs each block slower) and a select keeps
+        // the lanes k < m.
         if (i < kWave) {
             while (n > 1) {
                 const uint32_t m = (n + 1) / 2;
@@ -117,9 +129,14 @@ __global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t*
                     L[w] = __shfl(P[w], (int)((2 * i) & (kWave - 1)));
                     R[w] = __shfl(P[w], (int)((2 * i + 1) & (kWave - 1)));
                 }
-                if (i < m) {
+                if (Threads > kThreads) {
+                    uint32_t Z[NW];
+                    T::node_hash(L, R, Z, tab);
+                    const bool pair = i < m && 2 * i + 1 < n, single = i < m && 2 * i + 1 >= n;
+                    for (int w = 0; w < NW; ++w) P[w] = pair ? Z[w] : single ? L[w] : P[w];
+                } else if (i < m) {
                     if (2 * i + 1 < n)
-                        T::node_hash(L, R, P);
+                        T::node_hash(L, R, P, tab);
                     else
                         for (int w = 0; w < NW; ++w) P[w] = L[w];
                 }
@@ -132,29 +149,114 @@ __global__ void __launch_bounds__(kThreads, 4) merkle_tile_kernel(const uint8_t*
 }
 
 // A launch over a level of 2^18 entries or more (the host plans which):
-// lane g reduces group g of its segment -- entries [8t, min(8t + 8, c)) for
-// the segment's t-th group, c its entry count -- to one node in registers,
+// group g of its segment -- entries [8t, min(8t + 8, c)) for the segment's
+// t-th group, c its entry count -- is reduced to one node in registers,
 // forming the leaf hashes first in leaf mode.  Groups start at multiples of
 // 8, so, as with tiles, the promotion of a short last group is the whole
-// tree's.  The entries go through a stack of perfect subtrees: entry j is
-// merged with the subtrees of the trailing one bits of j (a binary counter),
-// and a short group folds what is left, smallest subtree first, which is
-// RFC 6962's split at the largest power of two.  Every lane of a wave works
-// on the widest levels, with no barrier and no LDS; the loops stay rolled
-// (one leaf-hash and one node-hash site), and stack slots are picked with
-// selects so that the stack stays in registers.  An empty segment has one
-// group, the hash of no entries.
+// tree's.  An empty segment has one group, the hash of no entries.
+//
+// Groups g < n_main take one lane each (blocks below main_blocks).  The
+// entries go through a stack of perfect subtrees: entry j is merged with the
+// subtrees of the trailing one bits of j (a binary counter), and a short
+// group folds what is left, smallest subtree first, which is RFC 6962's split
+// at the largest power of two.  Every lane of a wave works on the widest
+// levels, with no barrier and no LDS exchange; the loops stay rolled (one
+// leaf-hash and one node-hash site), and stack slots are picked with selects
+// so that the stack stays in registers.
+//
+// The launch's last groups, g >= n_main, take four lanes each (the blocks
+// after main_blocks): lane q forms the node of entries 2q and 2q + 1, then
+// two levels pair lanes (q, q + 1) and (0, 2) through cross-lane shuffles.
+// A wave then needs a third of the time per group that a one-lane wave
+// needs, which shortens the launch's last round (the host sizes n_main to
+// whole rounds of the chip's SIMDs).
 template <class T>
-__global__ void __launch_bounds__(kThreads) merkle_group_kernel(const uint8_t* __restrict__ in,
-                                                                 uint8_t* __restrict__ out,
-                                                                 const uint64_t* __restrict__ in_off,
-                                                                 const uint64_t* __restrict__ grp_off, uint32_t n_seg,
-                                                                 uint64_t n_groups, int leaf_mode) {
+__global__ void __launch_bounds__(kThreads, 4) merkle_group_kernel(const uint8_t* __restrict__ in,
+                                                                    uint8_t* __restrict__ out,
+                                                                    const uint64_t* __restrict__ in_off,
+                                                                    const uint64_t* __restrict__ grp_off,
+                                                                    uint32_t n_seg, uint64_t n_groups,
+                                                                    uint64_t n_main, uint32_t main_blocks,
+                                                                    int leaf_mode) {
     constexpr int NW = T::kWords;
     constexpr int NB = T::kBytes;
     constexpr int L = kGroupLevels;
-    for (uint64_t g = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; g < n_groups;
-         g += (uint64_t)gridDim.x * blockDim.x) {
+    __shared__ __align__(16) uint32_t tab[T::kTableWords];
+    T::stage_table(tab);
+    __syncthreads();
+    if (blockIdx.x < main_blocks) {
+        for (uint64_t g = (uint64_t)blockIdx.x * kThreads + threadIdx.x; g < n_main;
+             g += (uint64_t)main_blocks * kThreads) {
+            const uint32_t s = find_segment(grp_off, n_seg, g);
+            const uint64_t t = g - grp_off[s];
+            const uint64_t c = in_off[s + 1] - in_off[s];
+            const uint64_t first = t * kGroupNodes;
+            const uint32_t cnt =
+                c > first ? (uint32_t)(c - first < (uint64_t)kGroupNodes ? c - first : kGroupNodes) : 0u;
+            const uint8_t* base = in + NB * (in_off[s] + first);
+            uint32_t S[L][NW];  // S[l]: the perfect subtree of 2^l entries waiting for its right sibling
+            uint32_t X[NW];
+#pragma unroll
+            for (int l = 0; l < L; ++l)
+                for (int w = 0; w < NW; ++w) S[l][w] = 0;
+            if (cnt == 0) T::empty_hash(X);
+#pragma nounroll
+            for (uint32_t j = 0; j < cnt; ++j) {
+                uint32_t A[NW];
+                T::load(base + NB * j, A);
+                if (leaf_mode) T::leaf_hash(A, X); else for (int w = 0; w < NW; ++w) X[w] = A[w];
+                uint32_t l = 0;
+#pragma nounroll
+                while (l < (uint32_t)L && ((j >> l) & 1u)) {
+                    uint32_t Y[NW], Z[NW];
+                    for (int w = 0; w < NW; ++w) {
+                        uint32_t v = S[0][w];
+#pragma unroll
+                        for (int q = 1; q < L; ++q) v = l == (uint32_t)q ? S[q][w] : v;
+                        Y[w] = v;
+                    }
+                    T::node_hash(Y, X, Z, tab);
+                    for (int w = 0; w < NW; ++w) X[w] = Z[w];
+                    ++l;
+                }
+#pragma unroll
+                for (int q = 0; q < L; ++q)
+                    for (int w = 0; w < NW; ++w) S[q][w] = l == (uint32_t)q ? X[w] : S[q][w];
+            }
+            if (cnt > 0 && cnt < (uint32_t)kGroupNodes) {
+                bool have = false;
+#pragma nounroll
+                for (uint32_t l = 0; l < (uint32_t)L; ++l) {
+                    if (!((cnt >> l) & 1u)) continue;
+                    uint32_t Y[NW];
+                    for (int w = 0; w < NW; ++w) {
+                        uint32_t v = S[0][w];
+#pragma unroll
+                        for (int q = 1; q < L; ++q) v = l == (uint32_t)q ? S[q][w] : v;
+                        Y[w] = v;
+                    }
+                    if (!have) {
+                        for (int w = 0; w < NW; ++w) X[w] = Y[w];
+                        have = true;
+                    } else {
+                        uint32_t Z[NW];
+                        T::node_hash(Y, X, Z, tab);
+                        for (int w = 0; w < NW; ++w) X[w] = Z[w];
+                    }
+                }
+            }
+            T::store(out + NB * g, X);
+        }
+        return;
+    }
+    // Four lanes per group.  The four lanes of a quad share g, so they enter
+    // and leave the loop together and every shuffle reads a lane of the same
+    // group.
+    constexpr uint32_t Q = kGroupQuad;
+    const uint32_t q = threadIdx.x % Q;
+    const uint64_t quads = (uint64_t)(gridDim.x - main_blocks) * (kThreads / Q);
+    for (uint64_t g = n_main + (uint64_t)(blockIdx.x - main_blocks) * (kThreads / Q) + threadIdx.x / Q; g < n_groups;
+         g += quads) {
         const uint32_t s = find_segment(grp_off, n_seg, g);
         const uint64_t t = g - grp_off[s];
         const uint64_t c = in_off[s + 1] - in_off[s];
@@ -162,86 +264,90 @@ __global__ void __launch_bounds__(kThreads) merkle_group_kernel(const uint8_t* _
         const uint32_t cnt =
             c > first ? (uint32_t)(c - first < (uint64_t)kGroupNodes ? c - first : kGroupNodes) : 0u;
         const uint8_t* base = in + NB * (in_off[s] + first);
-        uint32_t S[L][NW];  // S[l]: the perfect subtree of 2^l entries waiting for its right sibling
-        uint32_t X[NW];
-#pragma unroll
-        for (int l = 0; l < L; ++l)
-            for (int w = 0; w < NW; ++w) S[l][w] = 0;
-        if (cnt == 0) T::empty_hash(X);
+        // N: this lane's entry 2q (then its node); X: entry 2q + 1.  Lanes
+        // past the group's end keep zeros.
+        uint32_t N[NW], X[NW];
+        for (int w = 0; w < NW; ++w) N[w] = X[w] = 0;
+        if (cnt == 0 && q == 0) T::empty_hash(N);
 #pragma nounroll
-        for (uint32_t j = 0; j < cnt; ++j) {
-            uint32_t A[NW];
-            T::load(base + NB * j, A);
-            if (leaf_mode) T::leaf_hash(A, X); else for (int w = 0; w < NW; ++w) X[w] = A[w];
-            uint32_t l = 0;
-#pragma nounroll
-            while (l < (uint32_t)L && ((j >> l) & 1u)) {
-                uint32_t Y[NW], Z[NW];
-                for (int w = 0; w < NW; ++w) {
-                    uint32_t v = S[0][w];
-#pragma unroll
-                    for (int q = 1; q < L; ++q) v = l == (uint32_t)q ? S[q][w] : v;
-                    Y[w] = v;
-                }
-                T::node_hash(Y, X, Z);
-                for (int w = 0; w < NW; ++w) X[w] = Z[w];
-                ++l;
+        for (uint32_t j = 0; j < 2; ++j) {
+            const uint32_t e = 2 * q + j;
+            uint32_t Y[NW] = {};
+            if (e < cnt) {
+                uint32_t A[NW];
+                T::load(base + NB * e, A);
+                if (leaf_mode) T::leaf_hash(A, Y); else for (int w = 0; w < NW; ++w) Y[w] = A[w];
             }
-#pragma unroll
-            for (int q = 0; q < L; ++q)
-                for (int w = 0; w < NW; ++w) S[q][w] = l == (uint32_t)q ? X[w] : S[q][w];
-        }
-        if (cnt > 0 && cnt < (uint32_t)kGroupNodes) {
-            bool have = false;
-#pragma nounroll
-            for (uint32_t l = 0; l < (uint32_t)L; ++l) {
-                if (!((cnt >> l) & 1u)) continue;
-                uint32_t Y[NW];
-                for (int w = 0; w < NW; ++w) {
-                    uint32_t v = S[0][w];
-#pragma unroll
-                    for (int q = 1; q < L; ++q) v = l == (uint32_t)q ? S[q][w] : v;
-                    Y[w] = v;
-                }
-                if (!have) {
-                    for (int w = 0; w < NW; ++w) X[w] = Y[w];
-                    have = true;
-                } else {
-                    uint32_t Z[NW];
-                    T::node_hash(Y, X, Z);
-                    for (int w = 0; w < NW; ++w) X[w] = Z[w];
-                }
+            for (int w = 0; w < NW; ++w) {
+                N[w] = j == 0 && e < cnt ? Y[w] : N[w];
+                X[w] = j == 1 && e < cnt ? Y[w] : X[w];
             }
         }
-        T::store(out + NB * g, X);
+        // Level l + 1 from level l: the left node's lane q is a multiple of
+        // 2^l; its right sibling is this lane's entry 2q + 1 (l = 0) or the
+        // node of lane q + 2^(l-1), which exists when its first entry,
+        // 2q + 1 or 2(q + 2^(l-1)), is in the group.
+#pragma nounroll
+        for (uint32_t l = 0; l < (uint32_t)L; ++l) {
+            const uint32_t d = l == 0 ? 1u : 1u << (l - 1);
+            uint32_t R[NW];
+            for (int w = 0; w < NW; ++w) {
+                const uint32_t v = (uint32_t)__shfl_xor((int)N[w], (int)d, (int)Q);
+                R[w] = l == 0 ? X[w] : v;
+            }
+            const bool left = (q & ((1u << l) - 1u)) == 0;
+            const uint32_t right_first = l == 0 ? 2 * q + 1 : 2 * (q + d);
+            if (left && right_first < cnt) {
+                uint32_t Z[NW];
+                T::node_hash(N, R, Z, tab);
+                for (int w = 0; w < NW; ++w) N[w] = Z[w];
+            }
+        }
+        if (q == 0) T::store(out + NB * g, N);
     }
 }
 
 }  // namespace
 
 hipError_t launch_merkle_groups(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
-                                const uint64_t* grp_off, uint32_t n_seg, uint64_t n_groups, int leaf_mode,
-                                hipStream_t s) {
+                                const uint64_t* grp_off, uint32_t n_seg, uint64_t n_groups, uint64_t n_main,
+                                int leaf_mode, hipStream_t s) {
     if (n_groups == 0) return hipSuccess;
-    const uint64_t blocks = (n_groups + kThreads - 1) / kThreads;
-    const unsigned grid = (unsigned)(blocks < (1u << 20) ? blocks : (1u << 20));
+    if (n_main > n_groups) return hipErrorInvalidValue;
+    const uint64_t cap = 1u << 19;  // blocks per part; both parts loop over their groups
+    const uint64_t mb = (n_main + kThreads - 1) / kThreads;
+    const uint64_t fb = ((n_groups - n_main) * kGroupQuad + kThreads - 1) / kThreads;
+    const uint32_t main_blocks = (uint32_t)(mb < cap ? mb : cap);
+    const unsigned grid = main_blocks + (unsigned)(fb < cap ? fb : cap);
     if (alg == kAlgSha384)
-        merkle_group_kernel<Sha384Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, grp_off, n_seg, n_groups, leaf_mode);
+        merkle_group_kernel<Sha384Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, grp_off, n_seg, n_groups, n_main,
+                                                                   main_blocks, leaf_mode);
     else
-        merkle_group_kernel<Sha256Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, grp_off, n_seg, n_groups, leaf_mode);
+        merkle_group_kernel<Sha256Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, grp_off, n_seg, n_groups, n_main,
+                                                                   main_blocks, leaf_mode);
     return hipGetLastError();
 }
 
 hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
-                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode,
+                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode, int wide,
                                hipStream_t s) {
     if (n_tiles == 0) return hipSuccess;
     const uint64_t cap = 1u << 20;
     const unsigned grid = (unsigned)(n_tiles < cap ? n_tiles : cap);
-    if (alg == kAlgSha384)
-        merkle_tile_kernel<Sha384Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
-    else
-        merkle_tile_kernel<Sha256Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
+    constexpr int W = 2 * kThreads;
+    if (alg == kAlgSha384) {
+        if (wide)
+            merkle_tile_kernel<Sha384Tree, W><<<grid, W, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
+        else
+            merkle_tile_kernel<Sha384Tree, kThreads>
+                <<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
+    } else {
+        if (wide)
+            merkle_tile_kernel<Sha256Tree, W><<<grid, W, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
+        else
+            merkle_tile_kernel<Sha256Tree, kThreads>
+                <<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
+    }
     return hipGetLastError();
 }
 

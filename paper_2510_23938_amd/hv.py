@@ -49,7 +49,7 @@ EXPORTS = (
     "hv_merkle_reduce", "hv_verify_workspace_bytes", "hv_verify_root", "hv_compare_roots",
     "hv_hash_chunks_alg", "hv_merkle_workspace_bytes_alg", "hv_merkle_reduce_alg", "hv_verify_root_alg",
     "hv_compare_roots_alg", "hv_hash_chunks_noalloc", "hv_last_error", "hv_set_kernel_timing", "hv_leaf_kernel_ms",
-    "hv_leaf_schedule", "hv_set_leaf_kernel", "hv_leaf_kernel_for",  # include/hv_inspect.h
+    "hv_leaf_schedule", "hv_set_leaf_kernel", "hv_leaf_kernel_for", "hv_merkle_launches",  # include/hv_inspect.h
     "hv_mb_valu", "hv_mb_sha256", "hv_mb_valu64", "hv_mb_sha384", "hv_mb_op_rate",
     "hv_mb_hbm_read",  # include/hv_microbench.h
     "hv_stream_workspace_bytes", "hv_hash_host_chunks", "hv_hash_host_chunks_alg",  # include/hv_stream.h
@@ -126,6 +126,8 @@ def _load():
         "hv_leaf_schedule": ([vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
         "hv_set_leaf_kernel": ([ctypes.c_int], ctypes.c_int),
         "hv_leaf_kernel_for": ([ctypes.c_uint64, ctypes.c_void_p], ctypes.c_int),
+        "hv_merkle_launches": ([ctypes.c_int32, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
+                                ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
         "hv_mb_valu": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_hbm_read": ([vp, u64, vp, u32, vp], ctypes.c_int),
         "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
@@ -589,6 +591,22 @@ def leaf_kernel_for(n_leaves: int) -> str:
     k = ctypes.c_int(0)
     _check(lib.hv_leaf_kernel_for(int(n_leaves), ctypes.byref(k)))
     return {1: "one-wave", 2: "two-wave", 3: "two-wave-compact"}[k.value]
+
+
+def merkle_launches(seg_offsets, alg: str = "sha256") -> list:
+    """The launches hv_merkle_reduce makes for these segments on the current device, as
+    (kind, units, one_lane) per launch: kind "group", "tile" or "wide-tile", the groups or tiles it reduces,
+    and the groups a group launch gives one lane each (its last units - one_lane groups take four);
+    kind "wide-tile" is a 1024-node tile launch."""
+    code, _ = _alg(alg)
+    seg = np.ascontiguousarray(seg_offsets, dtype=np.uint64)
+    if len(seg) < 2:
+        raise ValueError("seg_offsets needs at least two entries (one segment)")
+    n = ctypes.c_int(0)
+    kind = (ctypes.c_int * 8)()
+    units, one = (ctypes.c_uint64 * 8)(), (ctypes.c_uint64 * 8)()
+    _check(lib.hv_merkle_launches(code, seg.ctypes.data, len(seg) - 1, ctypes.byref(n), kind, units, one))
+    return [({1: "group", 2: "tile", 3: "wide-tile"}[kind[k]], int(units[k]), int(one[k])) for k in range(n.value)]
 
 
 def set_kernel_timing(enable: bool):

@@ -416,6 +416,30 @@ def test_leaf_kernel_choice_is_validated():
     assert hv.lib.hv_leaf_kernel_for(10, None) == hv.HV_ERR_INVALID_ARG
 
 
+def test_merkle_launch_plan_checks_its_arguments():
+    seg = np.array([0, 5, 9], dtype=np.uint64)
+    n = ctypes.c_int(0)
+    kind = (ctypes.c_int * 8)()
+    units, one = (ctypes.c_uint64 * 8)(), (ctypes.c_uint64 * 8)()
+    f = hv.lib.hv_merkle_launches
+    assert f(7, seg.ctypes.data, 2, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert f(hv.HV_SHA256, seg.ctypes.data, 0, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert f(hv.HV_SHA256, None, 2, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    for i in range(3):
+        args = [kind, units, one]
+        args[i] = None
+        assert f(hv.HV_SHA256, seg.ctypes.data, 2, ctypes.byref(n), *args) == hv.HV_ERR_INVALID_ARG
+    assert f(hv.HV_SHA256, seg.ctypes.data, 2, None, kind, units, one) == hv.HV_ERR_INVALID_ARG
+    bad = np.array([1, 5, 9], dtype=np.uint64)
+    assert f(hv.HV_SHA256, bad.ctypes.data, 2, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert b"not 0" in hv.lib.hv_last_error()
+    down = np.array([0, 5, 4], dtype=np.uint64)
+    assert f(hv.HV_SHA384, down.ctypes.data, 2, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert b"decreases" in hv.lib.hv_last_error()
+    with pytest.raises(ValueError):
+        hv.merkle_launches([0])
+
+
 def test_noalloc_refuses_what_its_static_scratch_cannot_hold():
     # the array's size as the header states it, and the largest single-message set it holds
     hdr = open(os.path.join(ROOT, "include", "hv.h")).read()

@@ -190,6 +190,73 @@ def test_merkle_two_group_launches_every_segment_size(alg):
     assert not bad, f"{alg}: roots differ for segment sizes {bad[:10]}"
 
 
+@pytest.mark.parametrize("alg", ["sha256", "sha384"])
+def test_merkle_four_lane_groups_every_segment_size(alg):
+    # A group launch gives its last groups four lanes each once the rest fill
+    # whole rounds of one wave per SIMD (256 groups per compute unit).  A first
+    # segment of exactly 64 such rounds' entries makes the one-lane part of
+    # both group launches end where the segments of sizes 0..600 begin, so the
+    # four-lane form meets every short group, in leaf mode (launch 1) and on
+    # level-3 nodes (launch 2); every root against the oracle.
+    D = 32 if alg == "sha256" else 48
+    cus = torch.cuda.get_device_properties(DEV).multi_processor_count
+    rnd = 256 * cus
+    small = list(range(601))
+    sizes = [64 * rnd] + small
+    n = sum(sizes)
+    seg = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    plan = hv.merkle_launches(seg, alg)
+    groups1 = sum(max(1, -(-c // 8)) for c in sizes)
+    groups2 = sum(max(1, -(-max(1, -(-c // 8)) // 8)) for c in sizes)
+    assert plan[0] == ("group", groups1, 8 * rnd), plan
+    assert plan[1] == ("group", groups2, rnd), plan
+    entries = W.random_bytes(n * D, 290 + D, DEV).view(n, D)
+    roots = hv.hv_merkle_reduce(entries, seg, alg=alg)
+    torch.cuda.synchronize()
+    host = entries.cpu().numpy()
+    want = [oracle.mth(host[int(seg[k]):int(seg[k + 1])], alg) for k in range(len(sizes))]
+    got = [bytes(r) for r in roots.cpu().numpy()]
+    bad = [sizes[k] for k in range(len(sizes)) if got[k] != want[k]]
+    assert not bad, f"{alg}: roots differ for segment sizes {bad[:10]}"
+
+
+@pytest.mark.parametrize("alg", ["sha256", "sha384"])
+def test_merkle_single_trees_of_500_to_1100_entries(alg):
+    # one segment of 513..1024 entries is one 1024-node tile (ten levels, one
+    # launch); 512 and 1025 and beyond take 512-node tiles
+    D = 32 if alg == "sha256" else 48
+    entries = W.random_bytes(1100 * D, 295 + D, DEV).view(1100, D)
+    host = entries.cpu().numpy()
+    ws = hv.Workspace(DEV)
+    bad = []
+    for n in range(500, 1101):
+        seg = np.array([0, n], dtype=np.uint64)
+        kinds = [p[0] for p in hv.merkle_launches(seg, alg)]
+        assert kinds == (["wide-tile"] if 512 < n <= 1024 else ["tile"] if n <= 512 else ["tile", "tile"]), (n, kinds)
+        root = hv.hv_merkle_reduce(entries[:n], seg, ws, alg=alg)
+        if bytes(root.cpu().numpy().reshape(-1)) != oracle.mth(host[:n], alg):
+            bad.append(n)
+    assert not bad, f"{alg}: roots differ for tree sizes {bad[:10]}"
+
+
+def test_merkle_launch_plan_of_the_70b_set():
+    # the 723 per-tensor trees of the 70B-shaped set: two group launches (the
+    # first with its last groups on four lanes when the rest fill whole
+    # rounds), then tiles
+    lens = W.workload_lengths(5)
+    leaves = [-(-int(L) // 65536) for L in lens]
+    seg = np.concatenate([[0], np.cumsum(leaves)]).astype(np.uint64)
+    rnd = 256 * torch.cuda.get_device_properties(DEV).multi_processor_count
+    plan = hv.merkle_launches(seg)
+    assert [p[0] for p in plan] == ["group", "group", "tile"], plan
+    kind, units, one = plan[0]
+    assert units == sum(-(-c // 8) for c in leaves)
+    assert one == units or (one % rnd == 0 and units - one < rnd), plan
+    assert plan[1][2] == plan[1][1]  # under one round: every group on one lane
+    # the manifest over the 723 roots: one 1024-node tile
+    assert hv.merkle_launches(np.array([0, len(leaves)], dtype=np.uint64)) == [("wide-tile", 1, 0)]
+
+
 @pytest.mark.parametrize("n", [(1 << 18) - 1, 1 << 18, (1 << 18) + 1, (1 << 18) + 7, 3 * (1 << 18) + 5,
                                (1 << 21) - 8, (1 << 21) - 7, (1 << 21) + 1])
 def test_merkle_single_tree_around_the_group_threshold(n):
