@@ -47,8 +47,9 @@ hv_status hv_set_leaf_kernel(int choice);
  * Errors: HV_ERR_INVALID_ARG for a NULL kernel. */
 hv_status hv_leaf_kernel_for(uint64_t n_leaves, int* kernel);
 
-/* The launches hv_merkle_reduce_alg makes for these segments on the current
- * device (RFC 6962 section 2.1's tree, built level by level; Algorithm 1's
+/* The launches hv_merkle_reduce_alg makes for these segments on a device of
+ * `cus` compute units, or on the current device when cus = 0 (RFC 6962
+ * section 2.1's tree, built level by level; Algorithm 1's
  * "construct Merkle tree from leaf_hashes using GPU"), for tests and
  * measurements: *launches (at most 8), and per launch k < *launches
  * kind[k] = 1 for a group launch (8 entries of a segment reduced by three
@@ -59,11 +60,12 @@ hv_status hv_leaf_kernel_for(uint64_t n_leaves, int* kernel);
  * group launch gives one lane each; its remaining units[k] - one_lane[k]
  * groups, the launch's last ones, take four lanes each (0 for a tile
  * launch).  kind, units and one_lane: host arrays of at least 8 entries.
- * Host only; no kernel runs.  Errors: HV_ERR_INVALID_ARG as
- * hv_merkle_reduce_alg's checks of alg and seg_offsets, or for a NULL output;
- * HV_ERR_HIP if the device cannot be queried. */
-hv_status hv_merkle_launches(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, int* launches, int* kind,
-                             uint64_t* units, uint64_t* one_lane);
+ * Host only; no kernel runs, and with cus > 0 no device is needed.
+ * Errors: HV_ERR_INVALID_ARG as hv_merkle_reduce_alg's checks of alg and
+ * seg_offsets, or for a NULL output; HV_ERR_HIP if cus = 0 and the current
+ * device cannot be queried. */
+hv_status hv_merkle_launches(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, uint32_t cus, int* launches,
+                             int* kind, uint64_t* units, uint64_t* one_lane);
 
 #ifdef __cplusplus
 }

@@ -306,20 +306,15 @@ hipError_t stream_cus(hipStream_t stream, uint32_t* cus) {
 
 }  // namespace
 
-hv_status merkle_launch_kinds(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, int dev, int* launches,
+hv_status merkle_launch_kinds(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, uint32_t cus, int* launches,
                               int* kind, uint64_t* units, uint64_t* one_lane) {
     std::vector<uint64_t> table;
     hv_status st = merkle_plan(seg_offsets, n_seg, &table, launches);
     if (st != HV_OK) return st;
     const size_t row = (size_t)n_seg + 1;
-    uint32_t cus = 0;
     for (int k = 1; k <= *launches; ++k) {
         const uint64_t entries = table[(size_t)(k - 1) * row + n_seg], out = table[(size_t)k * row + n_seg];
         const bool grouped = merkle_grouped(entries);
-        if (grouped && cus == 0) {
-            const hipError_t e = device_cus(dev, &cus);
-            if (e != hipSuccess) return hip_fail(e, "device query");
-        }
         kind[k - 1] = grouped ? 1 : merkle_wide(entries, n_seg) ? 3 : 2;
         units[k - 1] = out;
         one_lane[k - 1] = grouped ? merkle_group_main(out, k == 1, alg == HV_SHA384, cus) : 0;
@@ -683,18 +678,21 @@ hv_status hv_leaf_kernel_for(uint64_t n_leaves, int* kernel) {
     return HV_OK;
 }
 
-hv_status hv_merkle_launches(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, int* launches, int* kind,
-                             uint64_t* units, uint64_t* one_lane) {
+hv_status hv_merkle_launches(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, uint32_t cus, int* launches,
+                             int* kind, uint64_t* units, uint64_t* one_lane) {
     if (alg != HV_SHA256 && alg != HV_SHA384) return fail(HV_ERR_INVALID_ARG, "unknown algorithm %d", (int)alg);
     if (n_seg == 0) return fail(HV_ERR_INVALID_ARG, "n_seg is 0");
     if (seg_offsets == nullptr || launches == nullptr || kind == nullptr || units == nullptr || one_lane == nullptr)
         return fail(HV_ERR_INVALID_ARG, "seg_offsets, launches, kind, units and one_lane must be non-NULL");
     hv_status st = check_segments(seg_offsets, n_seg);
     if (st != HV_OK) return st;
-    int dev = -1;
-    const hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return hip_fail(e, "device query");
-    return merkle_launch_kinds(alg, seg_offsets, n_seg, dev, launches, kind, units, one_lane);
+    if (cus == 0) {
+        int dev = -1;
+        hipError_t e = hipGetDevice(&dev);
+        if (e == hipSuccess) e = device_cus(dev, &cus);
+        if (e != hipSuccess) return hip_fail(e, "device query");
+    }
+    return merkle_launch_kinds(alg, seg_offsets, n_seg, cus, launches, kind, units, one_lane);
 }
 
 hv_status hv_set_kernel_timing(int enable) {

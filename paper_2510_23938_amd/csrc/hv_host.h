@@ -102,9 +102,9 @@ hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<u
 // Segment offsets: start at 0, never decrease, at most the per-call entry limit.
 hv_status check_segments(const uint64_t* seg_offsets, uint32_t n_seg);
 
-// The launches a reduction of these (checked) segments makes on device `dev`
-// (hv_merkle_launches in hv_inspect.h).
-hv_status merkle_launch_kinds(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, int dev, int* launches,
+// The launches a reduction of these (checked) segments makes on a device of
+// `cus` compute units (hv_merkle_launches in hv_inspect.h).
+hv_status merkle_launch_kinds(hv_alg alg, const uint64_t* seg_offsets, uint32_t n_seg, uint32_t cus, int* launches,
                               int* kind, uint64_t* units, uint64_t* one_lane);
 
 // Groups a group launch of n_groups groups gives one lane each (the rest, its

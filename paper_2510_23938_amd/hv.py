@@ -126,8 +126,8 @@ def _load():
         "hv_leaf_schedule": ([vp, u32, u64, vp, vp, sz, vp], ctypes.c_int),
         "hv_set_leaf_kernel": ([ctypes.c_int], ctypes.c_int),
         "hv_leaf_kernel_for": ([ctypes.c_uint64, ctypes.c_void_p], ctypes.c_int),
-        "hv_merkle_launches": ([ctypes.c_int32, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
-                                ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+        "hv_merkle_launches": ([ctypes.c_int32, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_void_p,
+                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
         "hv_mb_valu": ([vp, u32, u32, vp, vp], ctypes.c_int),
         "hv_mb_hbm_read": ([vp, u64, vp, u32, vp], ctypes.c_int),
         "hv_mb_sha256": ([vp, u32, u32, vp, vp], ctypes.c_int),
@@ -593,8 +593,9 @@ def leaf_kernel_for(n_leaves: int) -> str:
     return {1: "one-wave", 2: "two-wave", 3: "two-wave-compact"}[k.value]
 
 
-def merkle_launches(seg_offsets, alg: str = "sha256") -> list:
-    """The launches hv_merkle_reduce makes for these segments on the current device, as
+def merkle_launches(seg_offsets, alg: str = "sha256", cus: int = 0) -> list:
+    """The launches hv_merkle_reduce makes for these segments on a device of ``cus`` compute units
+    (0: the current device), as
     (kind, units, one_lane) per launch: kind "group", "tile" or "wide-tile", the groups or tiles it reduces,
     and the groups a group launch gives one lane each (its last units - one_lane groups take four);
     kind "wide-tile" is a 1024-node tile launch."""
@@ -605,7 +606,7 @@ def merkle_launches(seg_offsets, alg: str = "sha256") -> list:
     n = ctypes.c_int(0)
     kind = (ctypes.c_int * 8)()
     units, one = (ctypes.c_uint64 * 8)(), (ctypes.c_uint64 * 8)()
-    _check(lib.hv_merkle_launches(code, seg.ctypes.data, len(seg) - 1, ctypes.byref(n), kind, units, one))
+    _check(lib.hv_merkle_launches(code, seg.ctypes.data, len(seg) - 1, int(cus), ctypes.byref(n), kind, units, one))
     return [({1: "group", 2: "tile", 3: "wide-tile"}[kind[k]], int(units[k]), int(one[k])) for k in range(n.value)]
 
 

@@ -292,8 +292,48 @@ static void rejections(void) {
     REJECTED(hv_stream_destroy(NULL), HV_ERR_INVALID_ARG);
 }
 
+/* Merkle launch plans over random segment sets and compute-unit counts: the
+ * launches end with one node per segment, every group launch's one-lane part
+ * is all of it or whole rounds of 256 groups per compute unit (and then less
+ * than one round remains), and a 1024-node tile only ends a one-segment tree. */
+static void merkle_plans(void) {
+    enum { MAXSEG = 300 };
+    static uint64_t seg[MAXSEG + 1];
+    for (int it = 0; it < 3000; ++it) {
+        const uint32_t n_seg = 1 + (uint32_t)(next() % MAXSEG);
+        const uint64_t scale = (uint64_t)1 << (next() % 23);
+        seg[0] = 0;
+        for (uint32_t i = 0; i < n_seg; ++i) seg[i + 1] = seg[i] + (next() % 5 == 0 ? 0 : next() % (2 * scale + 1));
+        const uint32_t cus = 1 + (uint32_t)(next() % 512);
+        int launches = 0, kind[8];
+        uint64_t units[8], one[8];
+        const hv_alg alg = (next() & 1) ? HV_SHA384 : HV_SHA256;
+        if (hv_merkle_launches(alg, seg, n_seg, cus, &launches, kind, units, one) != HV_OK) {
+            CHECK(seg[n_seg] > ((uint64_t)1 << 31)); /* only the entry limit may refuse a valid set */
+            continue;
+        }
+        CHECK(launches >= 1 && launches <= 8);
+        CHECK(units[launches - 1] == n_seg);
+        const uint64_t R = 256 * (uint64_t)cus;
+        for (int k = 0; k < launches; ++k) {
+            CHECK(kind[k] >= 1 && kind[k] <= 3);
+            CHECK(units[k] >= n_seg);
+            if (kind[k] == 1) CHECK(one[k] == units[k] || (one[k] % R == 0 && one[k] > 0 && units[k] - one[k] < R));
+            else CHECK(one[k] == 0);
+            if (kind[k] == 3) CHECK(n_seg == 1 && k == launches - 1);
+        }
+    }
+    /* no device is asked for when cus > 0; cus = 0 without one fails cleanly */
+    const uint64_t two[3] = {0, 5, 9};
+    int launches = 0, kind[8];
+    uint64_t units[8], one[8];
+    const hv_status st = hv_merkle_launches(HV_SHA256, two, 2, 0, &launches, kind, units, one);
+    CHECK(st == HV_OK || st == HV_ERR_HIP);
+}
+
 int main(void) {
     layouts_and_sizes();
+    merkle_plans();
     large_layouts();
     stream_plans();
     tree_sizes();

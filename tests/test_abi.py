@@ -422,22 +422,65 @@ def test_merkle_launch_plan_checks_its_arguments():
     kind = (ctypes.c_int * 8)()
     units, one = (ctypes.c_uint64 * 8)(), (ctypes.c_uint64 * 8)()
     f = hv.lib.hv_merkle_launches
-    assert f(7, seg.ctypes.data, 2, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
-    assert f(hv.HV_SHA256, seg.ctypes.data, 0, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
-    assert f(hv.HV_SHA256, None, 2, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert f(7, seg.ctypes.data, 2, 256, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert f(hv.HV_SHA256, seg.ctypes.data, 0, 256, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert f(hv.HV_SHA256, None, 2, 256, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
     for i in range(3):
         args = [kind, units, one]
         args[i] = None
-        assert f(hv.HV_SHA256, seg.ctypes.data, 2, ctypes.byref(n), *args) == hv.HV_ERR_INVALID_ARG
-    assert f(hv.HV_SHA256, seg.ctypes.data, 2, None, kind, units, one) == hv.HV_ERR_INVALID_ARG
+        assert f(hv.HV_SHA256, seg.ctypes.data, 2, 256, ctypes.byref(n), *args) == hv.HV_ERR_INVALID_ARG
+    assert f(hv.HV_SHA256, seg.ctypes.data, 2, 256, None, kind, units, one) == hv.HV_ERR_INVALID_ARG
     bad = np.array([1, 5, 9], dtype=np.uint64)
-    assert f(hv.HV_SHA256, bad.ctypes.data, 2, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert f(hv.HV_SHA256, bad.ctypes.data, 2, 256, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
     assert b"not 0" in hv.lib.hv_last_error()
     down = np.array([0, 5, 4], dtype=np.uint64)
-    assert f(hv.HV_SHA384, down.ctypes.data, 2, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
+    assert f(hv.HV_SHA384, down.ctypes.data, 2, 256, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
     assert b"decreases" in hv.lib.hv_last_error()
+    big = np.array([0, 1 << 40], dtype=np.uint64)
+    assert f(hv.HV_SHA256, big.ctypes.data, 1, 256, ctypes.byref(n), kind, units, one) == hv.HV_ERR_INVALID_ARG
     with pytest.raises(ValueError):
         hv.merkle_launches([0])
+
+
+def _groups(counts, w=8):
+    return sum(max(1, -(-int(c) // w)) for c in counts)
+
+
+@pytest.mark.parametrize("alg", ["sha256", "sha384"])
+def test_merkle_launch_plan_on_a_256_cu_device(alg):
+    # No device needed with an explicit compute-unit count.  The 70B-shaped
+    # set's 723 trees: the first group launch keeps 4 whole rounds of one wave
+    # per SIMD (256 groups per CU per round) on one lane and gives its last
+    # 7,153 groups four lanes; the second (34,000 groups, under a round) stays
+    # on one lane; a tile launch ends the trees.  The manifest is one 1024-node
+    # tile; the single tree of 10^6 entries keeps every group on one lane (its
+    # 125,000 groups are under two rounds, where the split would cost more).
+    import workloads as W
+    leaves = [-(-int(L) // 65536) for L in W.workload_lengths(5)]
+    seg = np.concatenate([[0], np.cumsum(leaves)]).astype(np.uint64)
+    g1 = _groups(leaves)
+    lvl3 = [max(1, -(-c // 8)) for c in leaves]
+    g2 = _groups(lvl3)
+    assert hv.merkle_launches(seg, alg, cus=256) == [("group", g1, 4 * 65536), ("group", g2, g2), ("tile", 723, 0)]
+    assert g1 - 4 * 65536 == 7153
+    assert hv.merkle_launches([0, 723], alg, cus=256) == [("wide-tile", 1, 0)]
+    assert hv.merkle_launches([0, 10 ** 6], alg, cus=256) == [("group", 125000, 125000), ("tile", 245, 0), ("tile", 1, 0)]
+
+
+def test_merkle_launch_plan_split_rule():
+    # the split is taken only where it shortens the busiest SIMD's work:
+    # k whole rounds of R = 256 * cus groups plus r more cost (k + 1) * D one
+    # lane each, or k * D + ceil(4r / R) * d with four-lane last groups
+    # (SHA-256: D = 22, d = 8 block times in leaf mode)
+    one = lambda n, cus: hv.merkle_launches([0, 8 * n], "sha256", cus=cus)[0]
+    R = 256 * 256
+    assert one(R + 1, 256) == ("group", R + 1, R)                  # 22 + 8 < 44: split
+    assert one(R + R // 2, 256) == ("group", R + R // 2, R)        # 22 + 16 < 44: split
+    assert one(R + R // 2 + 1, 256) == ("group", R + R // 2 + 1, R + R // 2 + 1)  # 22 + 24 >= 44: one lane
+    assert one(2 * R, 256) == ("group", 2 * R, 2 * R)              # whole rounds: nothing to split
+    assert one(R // 2 + 10000, 256)[2] == R // 2 + 10000           # under one round: one lane
+    # the rounds follow the compute-unit count
+    assert one(3 * 256 * 100 + 5, 100) == ("group", 3 * 256 * 100 + 5, 3 * 256 * 100)
 
 
 def test_noalloc_refuses_what_its_static_scratch_cannot_hold():
