@@ -53,9 +53,7 @@ hv_status hv_leaf_kernel_for(uint64_t n_leaves, int* kernel);
  * "construct Merkle tree from leaf_hashes using GPU"), for tests and
  * measurements: *launches (at most 8), and per launch k < *launches
  * kind[k] = 1 for a group launch (8 entries of a segment reduced by three
- * levels in registers), 2 for a tile launch (512 entries, nine levels) or 3
- * for a wide tile launch (1024 entries, ten levels: the last launch over one
- * segment of 513..1024 entries),
+ * levels in registers) or 2 for a tile launch (512 entries, nine levels),
  * units[k] = the groups or tiles it reduces, and one_lane[k] = the groups a
  * group launch gives one lane each; its remaining units[k] - one_lane[k]
  * groups, the launch's last ones, take four lanes each (0 for a tile

@@ -258,7 +258,7 @@ hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<u
     int k = 0;
     for (;;) {
         const uint64_t entries = (*table)[(size_t)k * row + n_seg];
-        const uint64_t w = merkle_width(entries, n_seg);
+        const uint64_t w = merkle_width(entries);
         std::vector<uint64_t> next(row);
         next[0] = 0;
         bool more = false;
@@ -315,7 +315,7 @@ hv_status merkle_launch_kinds(hv_alg alg, const uint64_t* seg_offsets, uint32_t 
     for (int k = 1; k <= *launches; ++k) {
         const uint64_t entries = table[(size_t)(k - 1) * row + n_seg], out = table[(size_t)k * row + n_seg];
         const bool grouped = merkle_grouped(entries);
-        kind[k - 1] = grouped ? 1 : merkle_wide(entries, n_seg) ? 3 : 2;
+        kind[k - 1] = grouped ? 1 : 2;
         units[k - 1] = out;
         one_lane[k - 1] = grouped ? merkle_group_main(out, k == 1, alg == HV_SHA384, cus) : 0;
     }
@@ -339,8 +339,7 @@ hv_status queue_merkle(hv_alg alg, const uint8_t* in, uint8_t* out, const uint64
             const uint64_t n_main = merkle_group_main(outputs[k - 1], k == 1, alg == HV_SHA384, cus);
             e = hv::launch_merkle_groups(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], n_main, k == 1, stream);
         } else {
-            e = hv::launch_merkle_tiles(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1,
-                                        merkle_wide(entries, n_seg), stream);
+            e = hv::launch_merkle_tiles(a, in, dst, in_off, out_off, n_seg, outputs[k - 1], k == 1, stream);
         }
         if (e != hipSuccess) return hip_fail(e, "merkle kernel");
         in = dst;

@@ -77,17 +77,9 @@ hv_status queue_schedule(const hv::MsgDesc* msgs_dev, uint32_t n_msgs, uint64_t 
 constexpr int kMaxMerkleLaunches = 8;
 constexpr uint64_t kGroupMinNodes = (uint64_t)1 << 18;
 inline bool merkle_grouped(uint64_t n_nodes) { return n_nodes >= kGroupMinNodes; }
-// A tile launch over one segment of 513..1024 entries takes one 1024-node
-// tile and finishes the tree, where 512-node tiles would need a second
-// launch for one level.
-inline bool merkle_wide(uint64_t n_nodes, uint32_t n_seg) {
-    return n_seg == 1 && n_nodes > (uint64_t)hv::kTileNodes && n_nodes <= (uint64_t)hv::kWideTileNodes;
-}
-// Entries one output node of a launch over n_nodes entries in n_seg segments covers.
-inline uint64_t merkle_width(uint64_t n_nodes, uint32_t n_seg) {
-    return merkle_grouped(n_nodes) ? (uint64_t)hv::kGroupNodes
-           : merkle_wide(n_nodes, n_seg) ? (uint64_t)hv::kWideTileNodes
-                                         : (uint64_t)hv::kTileNodes;
+// Entries one output node of a launch over n_nodes entries covers.
+inline uint64_t merkle_width(uint64_t n_nodes) {
+    return merkle_grouped(n_nodes) ? (uint64_t)hv::kGroupNodes : (uint64_t)hv::kTileNodes;
 }
 
 // Host plan of a segmented Merkle reduction over validated segment offsets:
@@ -95,8 +87,7 @@ inline uint64_t merkle_width(uint64_t n_nodes, uint32_t n_seg) {
 // the first output node of each segment after launch k (a segment with c
 // nodes gets max(1, ceil(c / w)) outputs, w = merkle_width(entries of row
 // k - 1)) -- and `launches` the launch count.  Launch k is a group launch
-// exactly when merkle_grouped(entries of row k - 1), and a wide tile launch
-// when merkle_wide(...).
+// exactly when merkle_grouped(entries of row k - 1).
 hv_status merkle_plan(const uint64_t* seg_offsets, uint32_t n_seg, std::vector<uint64_t>* table, int* launches);
 
 // Segment offsets: start at 0, never decrease, at most the per-call entry limit.

@@ -104,13 +104,11 @@ hipError_t launch_sha256_leaves(const LeafDesc* desc, uint64_t n_slots, uint64_t
 
 // Merkle tiles (merkle.hip).  One launch reduces every segment by up to
 // kTileLevels levels: tile t covers up to 2^kTileLevels consecutive nodes of
-// one segment and writes one node.  A wide launch takes tiles of
-// kWideTileNodes (one more level).
+// one segment and writes one node.
 constexpr int kTileLevels = 9;
 constexpr int kTileNodes = 1 << kTileLevels;
-constexpr int kWideTileNodes = 2 * kTileNodes;
 hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
-                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode, int wide,
+                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode,
                                hipStream_t s);
 // Merkle groups (merkle.hip), the launches over the widest levels: group g
 // -- up to 2^kGroupLevels consecutive nodes of one segment, starting at a

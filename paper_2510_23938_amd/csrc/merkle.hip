@@ -14,11 +14,15 @@
 // is the segment's last node there -- the same promotion the whole tree
 // makes.  One launch therefore takes every segment nine levels up; the host
 // chains such launches until one node per segment is left, and the first
-// launch of a reduction also forms the leaf hashes as it loads the entries.  Level 1 is formed in registers from the
-// two entries a thread loads.  Levels of more than 64 nodes go through LDS,
-// with idle waves waiting at the barriers; the last six levels of a full tile
-// (64 nodes down to one) stay in wave 0 and exchange children by cross-lane
-// shuffles.
+// launch of a reduction also forms the leaf hashes as it loads the entries.
+// Level 1 is formed in registers from the two entries a thread loads.  Levels
+// of more than 64 nodes go through LDS, with idle waves waiting at the
+// barriers; the last six levels of a full tile (64 nodes down to one) stay in
+// wave 0 and exchange children by cross-lane shuffles.  A wave with any node
+// to form hashes on all its lanes and keeps the needed results by selects:
+// the top levels are a chain of one wave's block latencies, and a wave with
+// few active lanes runs each block markedly slower (the per-tensor tops of
+// the 70B-shaped set: 57 us against 70).
 //
 // Levels of at least 2^18 entries run as group launches instead (below): one
 // lane per aligned group of 8 entries, three levels in registers, so that the
@@ -48,19 +52,16 @@ __device__ __forceinline__ uint32_t find_segment(const uint64_t* __restrict__ ti
     return lo;
 }
 
-// Tiles of 2 * Threads nodes: 512 (Threads = 256) in general, 1024 (512
-// threads) for a last launch over one segment of 513..1024 entries, which
-// then needs no second launch for its tenth level.  Four 512-node tiles per CU
-// where LDS allows (SHA-384 nodes); with SHA-256 the node-tail table (33 KB)
-// beside the 8 KB of level exchange leaves room for three.
-template <class T, int Threads>
-__global__ void __launch_bounds__(Threads, Threads > kThreads ? 1 : (T::kTableWords > 4 ? 3 : 4))
+// Four tiles per CU where LDS allows (SHA-384 nodes); with SHA-256 the
+// node-tail table (33 KB) beside the 8 KB of level exchange leaves room for three.
+template <class T>
+__global__ void __launch_bounds__(kThreads, T::kTableWords > 4 ? 3 : 4)
     merkle_tile_kernel(const uint8_t* __restrict__ in, uint8_t* __restrict__ out, const uint64_t* __restrict__ in_off,
                        const uint64_t* __restrict__ tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode) {
     constexpr int NW = T::kWords;
     constexpr int NB = T::kBytes;
-    constexpr uint32_t Nodes = 2 * Threads;
-    __shared__ uint32_t lds[NW][Threads];  // word-major: node i's word w at lds[w][i]
+    constexpr uint32_t Nodes = kTileNodes;
+    __shared__ uint32_t lds[NW][kThreads];  // word-major: node i's word w at lds[w][i]
     __shared__ __align__(16) uint32_t tab[T::kTableWords];
     const uint32_t i = threadIdx.x;
     T::stage_table(tab);
@@ -74,72 +75,69 @@ __global__ void __launch_bounds__(Threads, Threads > kThreads ? 1 : (T::kTableWo
         const uint8_t* base = in + NB * (in_off[s] + first);
 
         uint32_t P[NW] = {};  // lanes without a node feed zeros to the shuffles
-        uint32_t n;  // nodes held in lds after the first level
+        uint32_t n = 1;  // nodes of the current level (after the first)
         if (cnt == 0) {  // empty segment (only ever a first-launch tile)
             if (i == 0) T::empty_hash(P);
-            n = 1;
-        } else {
+        } else if ((i & ~(kWave - 1)) * 2 < cnt) {
+            // A wave that holds any node of level 1 hashes on every lane (a
+            // wave with few active lanes runs each block slower; it issues the
+            // same instructions either way): lanes past the tile's end take
+            // its last entry, and selects keep what the lane's own entries
+            // give -- a pair's node, an unpaired last node moved up, or none.
             const bool hasA = 2 * i < cnt, hasB = 2 * i + 1 < cnt;
-            uint32_t A[NW], B[NW];
-            if (hasA) {
-                T::load(base + 2 * NB * i, A);
-                if (leaf_mode) { uint32_t X[NW]; T::leaf_hash(A, X); for (int w = 0; w < NW; ++w) A[w] = X[w]; }
+            const uint32_t ea = hasA ? 2 * i : cnt - 1, eb = hasB ? 2 * i + 1 : cnt - 1;
+            uint32_t A[NW], B[NW], Z[NW];
+            T::load(base + NB * ea, A);
+            T::load(base + NB * eb, B);
+            if (leaf_mode) {
+                uint32_t X[NW];
+                T::leaf_hash(A, X);
+                for (int w = 0; w < NW; ++w) A[w] = X[w];
+                T::leaf_hash(B, X);
+                for (int w = 0; w < NW; ++w) B[w] = X[w];
             }
-            if (hasB) {
-                T::load(base + 2 * NB * i + NB, B);
-                if (leaf_mode) { uint32_t X[NW]; T::leaf_hash(B, X); for (int w = 0; w < NW; ++w) B[w] = X[w]; }
-                T::node_hash(A, B, P, tab);
-            } else if (hasA) {
-                for (int w = 0; w < NW; ++w) P[w] = A[w];  // unpaired last node moves up
-            }
-            n = (cnt + 1) / 2;
+            T::node_hash(A, B, Z, tab);
+            for (int w = 0; w < NW; ++w) P[w] = hasB ? Z[w] : hasA ? A[w] : 0u;
         }
+        if (cnt > 0) n = (cnt + 1) / 2;
         // Thread k now holds node k of the current level in P (k < n).  While
-        // the level spans more than one wave, children meet through LDS.
+        // the level spans more than one wave, children meet through LDS; as
+        // above, a wave with any parent to form hashes on every lane, reading
+        // in-bounds children, and a select keeps the lanes k < m.
         while (n > kWave) {
             const uint32_t m = (n + 1) / 2;
             if (i < n) for (int w = 0; w < NW; ++w) lds[w][i] = P[w];
             __syncthreads();
-            if (i < m) {
-                uint32_t L[NW];
-                for (int w = 0; w < NW; ++w) L[w] = lds[w][2 * i];
-                if (2 * i + 1 < n) {
-                    uint32_t R[NW];
-                    for (int w = 0; w < NW; ++w) R[w] = lds[w][2 * i + 1];
-                    T::node_hash(L, R, P, tab);
-                } else {
-                    for (int w = 0; w < NW; ++w) P[w] = L[w];
+            if ((i & ~(kWave - 1)) < m) {
+                const uint32_t a = 2 * i < n ? 2 * i : n - 1, b = 2 * i + 1 < n ? 2 * i + 1 : n - 1;
+                uint32_t L[NW], R[NW], Z[NW];
+                for (int w = 0; w < NW; ++w) {
+                    L[w] = lds[w][a];
+                    R[w] = lds[w][b];
                 }
+                T::node_hash(L, R, Z, tab);
+                const bool pair = i < m && 2 * i + 1 < n, single = i < m && 2 * i + 1 >= n;
+                for (int w = 0; w < NW; ++w) P[w] = pair ? Z[w] : single ? L[w] : P[w];
             }
             __syncthreads();  // every read of lds is done before the next level writes it
             n = m;
         }
         // The rest of the tile lies in wave 0's lanes: children come from
         // lanes 2k and 2k+1 by cross-lane shuffles, with no barrier.  Every
-        // lane of the wave takes part in the shuffles; only lanes k < m hash.
-        // A wide tile is a reduction's last launch, alone on the chip, where
-        // one wave's latency is the time: there every lane hashes (a wave
-        // with few active lanes runs each block slower) and a select keeps
-        // the lanes k < m.
+        // lane of the wave takes part in the shuffles and hashes (a wave with
+        // few active lanes runs each block slower, and the wave issues the
+        // same instructions either way); a select keeps the lanes k < m.
         if (i < kWave) {
             while (n > 1) {
                 const uint32_t m = (n + 1) / 2;
-                uint32_t L[NW], R[NW];
+                uint32_t L[NW], R[NW], Z[NW];
                 for (int w = 0; w < NW; ++w) {
                     L[w] = __shfl(P[w], (int)((2 * i) & (kWave - 1)));
                     R[w] = __shfl(P[w], (int)((2 * i + 1) & (kWave - 1)));
                 }
-                if (Threads > kThreads) {
-                    uint32_t Z[NW];
-                    T::node_hash(L, R, Z, tab);
-                    const bool pair = i < m && 2 * i + 1 < n, single = i < m && 2 * i + 1 >= n;
-                    for (int w = 0; w < NW; ++w) P[w] = pair ? Z[w] : single ? L[w] : P[w];
-                } else if (i < m) {
-                    if (2 * i + 1 < n)
-                        T::node_hash(L, R, P, tab);
-                    else
-                        for (int w = 0; w < NW; ++w) P[w] = L[w];
-                }
+                T::node_hash(L, R, Z, tab);
+                const bool pair = i < m && 2 * i + 1 < n, single = i < m && 2 * i + 1 >= n;
+                for (int w = 0; w < NW; ++w) P[w] = pair ? Z[w] : single ? L[w] : P[w];
                 n = m;
             }
             if (i == 0) T::store(out + NB * tile, P);
@@ -286,22 +284,22 @@ __global__ void __launch_bounds__(kThreads, 4) merkle_group_kernel(const uint8_t
         // Level l + 1 from level l: the left node's lane q is a multiple of
         // 2^l; its right sibling is this lane's entry 2q + 1 (l = 0) or the
         // node of lane q + 2^(l-1), which exists when its first entry,
-        // 2q + 1 or 2(q + 2^(l-1)), is in the group.
+        // 2q + 1 or 2(q + 2^(l-1)), is in the group.  Every lane hashes (these
+        // waves run at the end of the launch, where one wave's latency is the
+        // time, and a wave with few active lanes runs each block slower); a
+        // select keeps the pairs that exist.
 #pragma nounroll
         for (uint32_t l = 0; l < (uint32_t)L; ++l) {
             const uint32_t d = l == 0 ? 1u : 1u << (l - 1);
-            uint32_t R[NW];
+            uint32_t R[NW], Z[NW];
             for (int w = 0; w < NW; ++w) {
                 const uint32_t v = (uint32_t)__shfl_xor((int)N[w], (int)d, (int)Q);
                 R[w] = l == 0 ? X[w] : v;
             }
             const bool left = (q & ((1u << l) - 1u)) == 0;
             const uint32_t right_first = l == 0 ? 2 * q + 1 : 2 * (q + d);
-            if (left && right_first < cnt) {
-                uint32_t Z[NW];
-                T::node_hash(N, R, Z, tab);
-                for (int w = 0; w < NW; ++w) N[w] = Z[w];
-            }
+            T::node_hash(N, R, Z, tab);
+            for (int w = 0; w < NW; ++w) N[w] = left && right_first < cnt ? Z[w] : N[w];
         }
         if (q == 0) T::store(out + NB * g, N);
     }
@@ -329,25 +327,15 @@ hipError_t launch_merkle_groups(int alg, const uint8_t* in, uint8_t* out, const 
 }
 
 hipError_t launch_merkle_tiles(int alg, const uint8_t* in, uint8_t* out, const uint64_t* in_off,
-                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode, int wide,
+                               const uint64_t* tile_off, uint32_t n_seg, uint64_t n_tiles, int leaf_mode,
                                hipStream_t s) {
     if (n_tiles == 0) return hipSuccess;
     const uint64_t cap = 1u << 20;
     const unsigned grid = (unsigned)(n_tiles < cap ? n_tiles : cap);
-    constexpr int W = 2 * kThreads;
-    if (alg == kAlgSha384) {
-        if (wide)
-            merkle_tile_kernel<Sha384Tree, W><<<grid, W, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
-        else
-            merkle_tile_kernel<Sha384Tree, kThreads>
-                <<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
-    } else {
-        if (wide)
-            merkle_tile_kernel<Sha256Tree, W><<<grid, W, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
-        else
-            merkle_tile_kernel<Sha256Tree, kThreads>
-                <<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
-    }
+    if (alg == kAlgSha384)
+        merkle_tile_kernel<Sha384Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
+    else
+        merkle_tile_kernel<Sha256Tree><<<grid, kThreads, 0, s>>>(in, out, in_off, tile_off, n_seg, n_tiles, leaf_mode);
     return hipGetLastError();
 }
 

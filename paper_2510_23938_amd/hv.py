@@ -596,9 +596,8 @@ def leaf_kernel_for(n_leaves: int) -> str:
 def merkle_launches(seg_offsets, alg: str = "sha256", cus: int = 0) -> list:
     """The launches hv_merkle_reduce makes for these segments on a device of ``cus`` compute units
     (0: the current device), as
-    (kind, units, one_lane) per launch: kind "group", "tile" or "wide-tile", the groups or tiles it reduces,
-    and the groups a group launch gives one lane each (its last units - one_lane groups take four);
-    kind "wide-tile" is a 1024-node tile launch."""
+    (kind, units, one_lane) per launch: kind "group" or "tile", the groups or tiles it reduces,
+    and the groups a group launch gives one lane each (its last units - one_lane groups take four)."""
     code, _ = _alg(alg)
     seg = np.ascontiguousarray(seg_offsets, dtype=np.uint64)
     if len(seg) < 2:
@@ -607,7 +606,7 @@ def merkle_launches(seg_offsets, alg: str = "sha256", cus: int = 0) -> list:
     kind = (ctypes.c_int * 8)()
     units, one = (ctypes.c_uint64 * 8)(), (ctypes.c_uint64 * 8)()
     _check(lib.hv_merkle_launches(code, seg.ctypes.data, len(seg) - 1, int(cus), ctypes.byref(n), kind, units, one))
-    return [({1: "group", 2: "tile", 3: "wide-tile"}[kind[k]], int(units[k]), int(one[k])) for k in range(n.value)]
+    return [({1: "group", 2: "tile"}[kind[k]], int(units[k]), int(one[k])) for k in range(n.value)]
 
 
 def set_kernel_timing(enable: bool):

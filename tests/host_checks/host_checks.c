@@ -293,9 +293,9 @@ static void rejections(void) {
 }
 
 /* Merkle launch plans over random segment sets and compute-unit counts: the
- * launches end with one node per segment, every group launch's one-lane part
- * is all of it or whole rounds of 256 groups per compute unit (and then less
- * than one round remains), and a 1024-node tile only ends a one-segment tree. */
+ * launches end with one node per segment, and every group launch's one-lane
+ * part is all of it or whole rounds of 256 groups per compute unit (and then
+ * less than one round remains). */
 static void merkle_plans(void) {
     enum { MAXSEG = 300 };
     static uint64_t seg[MAXSEG + 1];
@@ -316,11 +316,10 @@ static void merkle_plans(void) {
         CHECK(units[launches - 1] == n_seg);
         const uint64_t R = 256 * (uint64_t)cus;
         for (int k = 0; k < launches; ++k) {
-            CHECK(kind[k] >= 1 && kind[k] <= 3);
+            CHECK(kind[k] == 1 || kind[k] == 2);
             CHECK(units[k] >= n_seg);
             if (kind[k] == 1) CHECK(one[k] == units[k] || (one[k] % R == 0 && one[k] > 0 && units[k] - one[k] < R));
             else CHECK(one[k] == 0);
-            if (kind[k] == 3) CHECK(n_seg == 1 && k == launches - 1);
         }
     }
     /* no device is asked for when cus > 0; cus = 0 without one fails cleanly */

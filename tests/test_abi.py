@@ -452,8 +452,8 @@ def test_merkle_launch_plan_on_a_256_cu_device(alg):
     # set's 723 trees: the first group launch keeps 4 whole rounds of one wave
     # per SIMD (256 groups per CU per round) on one lane and gives its last
     # 7,153 groups four lanes; the second (34,000 groups, under a round) stays
-    # on one lane; a tile launch ends the trees.  The manifest is one 1024-node
-    # tile; the single tree of 10^6 entries keeps every group on one lane (its
+    # on one lane; a tile launch ends the trees.  The manifest takes two tile
+    # launches; the single tree of 10^6 entries keeps every group on one lane (its
     # 125,000 groups are under two rounds, where the split would cost more).
     import workloads as W
     leaves = [-(-int(L) // 65536) for L in W.workload_lengths(5)]
@@ -463,7 +463,7 @@ def test_merkle_launch_plan_on_a_256_cu_device(alg):
     g2 = _groups(lvl3)
     assert hv.merkle_launches(seg, alg, cus=256) == [("group", g1, 4 * 65536), ("group", g2, g2), ("tile", 723, 0)]
     assert g1 - 4 * 65536 == 7153
-    assert hv.merkle_launches([0, 723], alg, cus=256) == [("wide-tile", 1, 0)]
+    assert hv.merkle_launches([0, 723], alg, cus=256) == [("tile", 2, 0), ("tile", 1, 0)]
     assert hv.merkle_launches([0, 10 ** 6], alg, cus=256) == [("group", 125000, 125000), ("tile", 245, 0), ("tile", 1, 0)]
 
 

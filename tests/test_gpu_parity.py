@@ -222,8 +222,8 @@ def test_merkle_four_lane_groups_every_segment_size(alg):
 
 @pytest.mark.parametrize("alg", ["sha256", "sha384"])
 def test_merkle_single_trees_of_500_to_1100_entries(alg):
-    # one segment of 513..1024 entries is one 1024-node tile (ten levels, one
-    # launch); 512 and 1025 and beyond take 512-node tiles
+    # one segment around the 512-node tile: one launch up to 512 entries, a
+    # second over the first launch's two or three tile nodes after it
     D = 32 if alg == "sha256" else 48
     entries = W.random_bytes(1100 * D, 295 + D, DEV).view(1100, D)
     host = entries.cpu().numpy()
@@ -232,7 +232,7 @@ def test_merkle_single_trees_of_500_to_1100_entries(alg):
     for n in range(500, 1101):
         seg = np.array([0, n], dtype=np.uint64)
         kinds = [p[0] for p in hv.merkle_launches(seg, alg)]
-        assert kinds == (["wide-tile"] if 512 < n <= 1024 else ["tile"] if n <= 512 else ["tile", "tile"]), (n, kinds)
+        assert kinds == (["tile"] if n <= 512 else ["tile", "tile"]), (n, kinds)
         root = hv.hv_merkle_reduce(entries[:n], seg, ws, alg=alg)
         if bytes(root.cpu().numpy().reshape(-1)) != oracle.mth(host[:n], alg):
             bad.append(n)
@@ -253,8 +253,8 @@ def test_merkle_launch_plan_of_the_70b_set():
     assert units == sum(-(-c // 8) for c in leaves)
     assert one == units or (one % rnd == 0 and units - one < rnd), plan
     assert plan[1][2] == plan[1][1]  # under one round: every group on one lane
-    # the manifest over the 723 roots: one 1024-node tile
-    assert hv.merkle_launches(np.array([0, len(leaves)], dtype=np.uint64)) == [("wide-tile", 1, 0)]
+    # the manifest over the 723 roots: a 512-node tile and a tile of two
+    assert hv.merkle_launches(np.array([0, len(leaves)], dtype=np.uint64)) == [("tile", 2, 0), ("tile", 1, 0)]
 
 
 @pytest.mark.parametrize("n", [(1 << 18) - 1, 1 << 18, (1 << 18) + 1, (1 << 18) + 7, 3 * (1 << 18) + 5,
